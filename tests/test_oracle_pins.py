@@ -1,0 +1,335 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each test ties one oracle function to something other than itself: numbers
+printed in Table 4, hand-worked tiny examples, brute-force enumeration, a
+library routine (PyTorch's CPU scaled-dot-product attention in fp64) on the
+special cases where the method reduces to plain attention, and closed forms.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import assembly, attention, cost, maxidf
+from paper_2607_20457_amd import workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- cost model --
+
+def _table4():
+    with open(os.path.join(GOLDEN, "table4.json")) as f:
+        return json.load(f)
+
+
+def test_table4_critical_lengths():
+    t = _table4()
+    for idx, L in enumerate(t["lengths"]):
+        n_p = cost.pulsar_len(L, t["B"], t["sink"], t["sigma"], t["B"] - 1)
+        assert n_p == t["critical_len"]["pulsar"][idx]
+        assert cost.star_len(L, t["B"]) == t["critical_len"]["star"][idx]
+        assert cost.dense_len(L) == t["critical_len"]["dense"][idx]
+        # the same count from Eq. 3 (one block + sink + 3 summaries of sigma rows)
+        assert assembly.phase1_len(L, t["B"], t["B"] - 1, t["sink"], 32, t["sigma"] // 32) == n_p
+        assert assembly.phase1_len(L, t["B"], t["B"] - 1, t["sink"], 32, 16,
+                                   assembly.PREFIX_ANCHOR) == cost.star_len(L, t["B"])
+
+
+def test_table4_flops_and_ratios():
+    t = _table4()
+    for idx, L in enumerate(t["lengths"]):
+        n = {m: t["critical_len"][m][idx] for m in ("dense", "star", "pulsar")}
+        F = {m: cost.table4_flops(n[m]) for m in n}
+        for m in ("star", "pulsar"):
+            assert round(F[m] / 1e9) == t["flops_G"][m][idx]
+        # printed 43,981 G at 64K dense vs 43,980.47 G: within one printed unit
+        assert abs(F["dense"] / 1e9 - t["flops_G"]["dense"][idx]) <= 1.0
+        assert round(F["star"] / F["pulsar"], 1) == t["flop_reduction_pulsar_vs_star"][idx]
+        assert round(F["dense"] / F["pulsar"], 1) == t["flop_reduction_vs_dense"]["pulsar"][idx]
+        assert round(F["dense"] / F["star"], 1) == t["flop_reduction_vs_dense"]["star"][idx]
+        # activation memory column: 20480 B per row, decimal MB for Pulsar
+        assert round(n["pulsar"] * 20480 / 1e6) == t["pulsar_act_mem_MB"][idx]
+
+
+def test_fixed_prefix_1600_tokens():
+    t = _table4()
+    n = cost.pulsar_len(16384, t["B"], t["sink"], t["sigma"], t["B"] - 1)
+    assert n - 16384 // t["B"] == t["prefix_tokens"]
+
+
+def test_host_critical_path():
+    # B=8 blocks on H=4 hosts, two consecutive blocks per host (Appendix
+    # "Block-to-Host Scalability Analysis"): the last host carries blocks 6,7.
+    lens = [cost.pulsar_len(131072, 8, 64, 2048, i) for i in range(8)]
+    pi = [i // 2 for i in range(8)]
+    C = cost.host_costs(lens, pi)
+    assert C[3] == cost.table4_flops(lens[6]) + cost.table4_flops(lens[7])
+    assert cost.critical_path(lens, pi) == C[3]
+
+
+def test_causal_pairs_closed_form():
+    for n in (1, 2, 7, 64):
+        brute = sum(1 for r in range(n) for c in range(n) if c <= r)
+        assert cost.causal_pairs(n) == brute
+    assert cost.causal_attn_flops(23616, 32, 128) == 4 * 128 * 32 * 23616 * 23617 // 2
+
+
+# ------------------------------------------------------------------- Max-IDF --
+
+# Hand-worked example: N = 3 blocks of 4 tokens, vocab 7 (token 6 absent).
+#   B0 = [5,5,1,2]   B1 = [1,3,3,3]   B2 = [1,2,4,0]
+#   df: 0->1, 1->3, 2->2, 3->1, 4->1, 5->1 (twice in B0, still one block), 6->0
+#   IDF = ln(3 / max(df,1)): ln3, 0, ln1.5, ln3, ln3, ln3, ln3
+#   chunks of 2: B0 [5,5]=ln3 [1,2]=ln1.5 | B1 [1,3]=ln3 [3,3]=ln3 | B2 [1,2]=ln1.5 [4,0]=ln3
+#   k = 1: B0 -> chunk 0, B1 -> tie -> lower index 0, B2 -> chunk 1
+HAND_IDS = [5, 5, 1, 2, 1, 3, 3, 3, 1, 2, 4, 0]
+
+
+def test_hand_example_df_idf():
+    df = maxidf.document_frequency(HAND_IDS, 3, 7)
+    assert df.tolist() == [1, 3, 2, 1, 1, 1, 0]
+    idf = maxidf.idf_table(df, 3)
+    l3, l15 = math.log(3.0), math.log(1.5)
+    np.testing.assert_allclose(idf, [l3, 0.0, l15, l3, l3, l3, l3], rtol=0, atol=1e-15)
+
+
+def test_hand_example_scores_and_selection():
+    sel, mindf, idf, scores = maxidf.maxidf_summaries(np.array([HAND_IDS]), 3, 2, 1, 7)
+    l3, l15 = math.log(3.0), math.log(1.5)
+    np.testing.assert_allclose(scores[0], [[l3, l15], [l3, l3], [l15, l3]], atol=1e-15)
+    assert mindf[0].tolist() == [[1, 2], [1, 1], [2, 1]]
+    assert sel[0].tolist() == [[0], [0], [1]]
+    sel2, _, _, _ = maxidf.maxidf_summaries(np.array([HAND_IDS]), 3, 2, 2, 7)
+    assert sel2[0].tolist() == [[0, 1], [0, 1], [0, 1]]
+
+
+def test_absent_tokens_get_ln_n():
+    # the max(df, 1) guard of Eq. idf: unseen ids score ln N, not +inf
+    ids = np.arange(64, dtype=np.int32) % 16
+    df = maxidf.document_frequency(ids, 4, 40)
+    idf = maxidf.idf_table(df, 4)
+    assert np.all(df[16:] == 0)
+    np.testing.assert_allclose(idf[16:], math.log(4.0), atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_maxidf_ranking_equals_mindf_ranking(seed):
+    # log is strictly decreasing in df >= 1, so (score desc, idx) == (mindf asc, idx)
+    for vocab, N, Lb, m in ((512, 8, 256, 16), (2048, 4, 128, 8), (64, 16, 64, 4)):
+        ids = workload.zipf_ids(seed, N * Lb, vocab)
+        df = maxidf.document_frequency(ids, N, vocab)
+        sc = maxidf.chunk_scores(ids, maxidf.idf_table(df, N), N, m)
+        md = maxidf.chunk_min_df(ids, df, N, m)
+        for j in range(N):
+            C = sc.shape[1]
+            by_score = sorted(range(C), key=lambda c: (-sc[j, c], c))
+            by_mindf = sorted(range(C), key=lambda c: (md[j, c], c))
+            assert by_score == by_mindf
+
+
+def _dominant_subsets(scores, k):
+    """All k-subsets whose members each beat every non-member on
+    (score desc, index asc), found by enumeration."""
+    C = len(scores)
+    better = lambda a, b: (scores[a] > scores[b]) or (scores[a] == scores[b] and a < b)
+    found = []
+    for sub in itertools.combinations(range(C), k):
+        rest = [c for c in range(C) if c not in sub]
+        if all(better(a, b) for a in sub for b in rest):
+            found.append(list(sub))
+    return found
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_topk_bruteforce_subsets(seed):
+    rng = np.random.default_rng(seed)
+    C = int(rng.integers(1, 11))
+    k = int(rng.integers(0, C + 1))
+    # few distinct values, so ties are common
+    scores = rng.integers(0, 4, size=C).astype(float)
+    subs = _dominant_subsets(scores, k)
+    assert len(subs) == 1
+    assert maxidf.select_topk(scores, k) == subs[0]
+
+
+def test_single_block_is_pure_tie_break():
+    # N = 1: every token has df = 1, IDF = ln 1 = 0, all chunks tie
+    ids = workload.zipf_ids(3, 512, 1000)
+    sel, mindf, idf, _ = maxidf.maxidf_summaries(ids[None], 1, 16, 5, 1000)
+    assert np.all(idf[0] == 0.0)
+    assert sel[0, 0].tolist() == [0, 1, 2, 3, 4]
+    assert np.all(mindf == 1)
+
+
+def test_needle_chunks_are_selected():
+    # Zipf over 512 ids: at 8 blocks of 4096 every background id is in
+    # several blocks, so a planted df = 1 needle is the unique best chunk
+    # while at most k needles share a block (Appendix "Max-IDF" strength).
+    cfg = workload.Config("t", L=32768, vocab=512, num_blocks=8, sink=64, chunk=32,
+                          topk=4, Hq=1, Hkv=1, d=64)
+    base = workload.zipf_ids(11, cfg.L, 512)
+    df0 = maxidf.document_frequency(base, 8, 600)
+    assert df0[:512][df0[:512] > 0].min() >= 2
+    ids, needles, pos = workload.plant_needles(12, base, 12, 600)
+    sel, mindf, _, _ = maxidf.maxidf_summaries(ids[None], 8, 32, 4, 600)
+    Lb = cfg.Lb
+    for p in pos:
+        j, c = p // Lb, (p % Lb) // 32
+        if np.sum(pos // Lb == j) <= 4:
+            assert c in sel[0, j].tolist()
+            assert mindf[0, j, c] == 1
+
+
+# ------------------------------------------------------------------ assembly --
+
+def test_positions_hand_example():
+    # L=32, N=4 (Lb=8), sink 2, chunk 2, k 2
+    sel = [[0, 3], [1, 2], [0, 1], [2, 3]]
+    pos = assembly.phase1_positions(32, 4, 2, 2, 2, 2, sel)
+    assert pos.tolist() == [0, 1,  0, 1, 6, 7,  10, 11, 12, 13] + list(range(16, 24))
+    assert len(pos) == assembly.phase1_len(32, 4, 2, 2, 2, 2)
+    assert assembly.phase1_positions(32, 4, 0, 2, 2, 2, sel).tolist() == list(range(8))
+    star = assembly.phase1_positions(32, 4, 3, 2, 2, 2, sel, assembly.PREFIX_ANCHOR)
+    assert star.tolist() == list(range(8)) + list(range(24, 32))
+    # no summaries and no sink: the block alone
+    assert assembly.phase1_positions(32, 4, 3, 0, 2, 0, [[]] * 4).tolist() == list(range(24, 32))
+
+
+def test_positions_structure_and_length_formula():
+    rng = np.random.default_rng(5)
+    L, N, s, m, k = 4096, 8, 64, 32, 3
+    Lb = L // N
+    sel = np.sort(np.stack([rng.choice(Lb // m, k, replace=False) for _ in range(N)]), axis=1)
+    for i in range(N):
+        pos = assembly.phase1_positions(L, N, i, s, m, k, sel)
+        sigma = k * m
+        n_formula = cost.pulsar_len(L, N, s, sigma, i) if i else Lb
+        assert len(pos) == n_formula
+        keep = assembly.retained_mask(len(pos), Lb)
+        assert pos[keep].tolist() == list(range(i * Lb, (i + 1) * Lb))
+        assert np.all(np.diff(pos[keep]) == 1)
+        if i:
+            assert pos[:s].tolist() == list(range(s))
+            runs = pos[s:s + i * sigma].reshape(i * k, m)
+            assert np.all(np.diff(runs, axis=1) == 1)
+            assert np.all(runs[:, 0] % m == 0)
+            assert (runs[:, 0] // Lb).tolist() == [j for j in range(i) for _ in range(k)]
+
+
+# ----------------------------------------------------------------- attention --
+
+def _sdpa(q, k, v, causal):
+    """PyTorch CPU fp64 SDPA on [n, H, d] inputs with grouped KV heads."""
+    qt = torch.from_numpy(np.asarray(q, dtype=np.float64)).transpose(0, 1)[None]
+    kt = torch.from_numpy(np.asarray(k, dtype=np.float64)).transpose(0, 1)[None]
+    vt = torch.from_numpy(np.asarray(v, dtype=np.float64)).transpose(0, 1)[None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=causal,
+                                                         enable_gqa=True)
+    return o[0].transpose(0, 1).numpy()
+
+
+@pytest.mark.parametrize("n,Hq,Hkv,d", [(37, 4, 1, 16), (80, 8, 2, 32), (130, 4, 4, 64)])
+def test_causal_attention_matches_sdpa(n, Hq, Hkv, d):
+    rng = np.random.default_rng(n)
+    q = rng.standard_normal((n, Hq, d))
+    k = rng.standard_normal((n, Hkv, d))
+    v = rng.standard_normal((n, Hkv, d))
+    o, lse = attention.causal_attention(q, k, v, 1 / math.sqrt(d), row_tile=32)
+    np.testing.assert_allclose(o, _sdpa(q, k, v, True), atol=1e-12, rtol=0)
+    rows = [0, 1, n // 2, n - 1]
+    o_r, lse_r = attention.causal_attention_rows(q, k, v, 1 / math.sqrt(d), rows)
+    np.testing.assert_allclose(o_r, o[rows], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse_r, lse[:, rows], atol=1e-12, rtol=0)
+
+
+def test_attention_closed_forms():
+    rng = np.random.default_rng(1)
+    n, Hq, Hkv, d = 50, 4, 2, 8
+    q = rng.standard_normal((n, Hq, d))
+    k = rng.standard_normal((n, Hkv, d))
+    v = rng.standard_normal((n, Hkv, d))
+    scale = 1 / math.sqrt(d)
+    o, lse = attention.causal_attention(q, k, v, scale)
+    # row 0 sees only key 0
+    for h in range(Hq):
+        np.testing.assert_allclose(o[0, h], v[0, h // 2], atol=1e-14)
+        assert abs(lse[h, 0] - scale * q[0, h] @ k[0, h // 2]) < 1e-13
+    # zero queries: uniform weights, O_r = mean(v_0..v_r), LSE_r = ln(r+1)
+    o0, lse0 = attention.causal_attention(np.zeros_like(q), k, v, scale)
+    for r in (0, 9, 49):
+        np.testing.assert_allclose(o0[r, 3], v[:r + 1, 1].mean(axis=0), atol=1e-13)
+        assert abs(lse0[3, r] - math.log(r + 1)) < 1e-13
+    # identical keys: every row averages its visible values
+    o1, _ = attention.causal_attention(q, np.repeat(k[:1], n, axis=0), v, scale)
+    np.testing.assert_allclose(o1[20, 0], v[:21, 0].mean(axis=0), atol=1e-13)
+
+
+def test_phase1_reduces_to_plain_causal():
+    rng = np.random.default_rng(2)
+    L, N, Hq, Hkv, d = 256, 4, 4, 2, 16
+    Q = rng.standard_normal((L, Hq, d))
+    K = rng.standard_normal((L, Hkv, d))
+    V = rng.standard_normal((L, Hkv, d))
+    Lb = L // N
+    # block 0 is [B_0]; sink 0 and k 0 leave [B_i]
+    for i, s, k in ((0, 8, 2), (2, 0, 0)):
+        pos = assembly.phase1_positions(L, N, i, s, 8, k, [[0, 1][:k]] * N)
+        o, _ = attention.phase1_attention(Q, K, V, pos, 0.25)
+        blk = slice(i * Lb, (i + 1) * Lb)
+        np.testing.assert_allclose(o, _sdpa(Q[blk], K[blk], V[blk], True), atol=1e-12)
+
+
+def test_partial_matches_sdpa_and_empty_shard():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((5, 8, 32))
+    K = rng.standard_normal((70, 2, 32))
+    V = rng.standard_normal((70, 2, 32))
+    o, lse = attention.partial_attention(q, K, V, 1 / math.sqrt(32))
+    np.testing.assert_allclose(o, _sdpa(q, K, V, False), atol=1e-12)
+    # q = 0: lse = ln S exactly
+    _, lse0 = attention.partial_attention(np.zeros_like(q), K, V, 0.3)
+    np.testing.assert_allclose(lse0, math.log(70), atol=1e-13)
+    oe, le = attention.partial_attention(q, K[:0], V[:0], 0.3)
+    assert np.all(oe == 0) and np.all(le == -np.inf)
+
+
+@pytest.mark.parametrize("H", [1, 2, 5, 16])
+def test_merge_equals_dense(H):
+    rng = np.random.default_rng(H)
+    Tq, Hq, Hkv, d, S = 3, 4, 2, 16, 24
+    q = rng.standard_normal((Tq, Hq, d)) * 2
+    K = rng.standard_normal((H * S, Hkv, d))
+    V = rng.standard_normal((H * S, Hkv, d))
+    scale = 1 / math.sqrt(d)
+    parts = [attention.partial_attention(q, K[h * S:(h + 1) * S], V[h * S:(h + 1) * S], scale)
+             for h in range(H)]
+    o, lse = attention.lse_merge(np.stack([p[0] for p in parts]), np.stack([p[1] for p in parts]))
+    od, lsed = attention.dense_attention(q, K, V, scale)
+    assert np.max(np.abs(o - od)) <= 1e-12
+    assert np.max(np.abs(lse - lsed)) <= 1e-12
+    if H == 1:
+        assert np.array_equal(o, parts[0][0]) and np.array_equal(lse, parts[0][1])
+
+
+def test_merge_skips_empty_and_survives_large_gaps():
+    rng = np.random.default_rng(9)
+    o_parts = rng.standard_normal((3, 2, 2, 4))
+    lse_parts = np.array([[[0.0, 1.0], [2.0, 3.0]],
+                          [[-np.inf] * 2] * 2,
+                          [[1000.0, -1000.0], [5.0, 2.0]]])
+    o, lse = attention.lse_merge(o_parts, lse_parts)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    # lse = log(e^a + e^c) written out for one entry without overflow
+    a, c = 2.0, 5.0
+    assert abs(lse[1, 0] - (c + math.log(1 + math.exp(a - c)))) < 1e-14
+    # a gap of 1000 leaves the larger partial alone
+    np.testing.assert_allclose(o[0, 0], o_parts[2, 0, 0], atol=1e-14)
+    np.testing.assert_allclose(o[1, 0], o_parts[0, 1, 0], atol=1e-14)
+    # dropping the empty shard changes nothing
+    o2, lse2 = attention.lse_merge(o_parts[[0, 2]], lse_parts[[0, 2]])
+    assert np.array_equal(o, o2) and np.array_equal(lse, lse2)
