@@ -1,0 +1,210 @@
+/*
+ * pulsar.h -- C ABI of the MI355X (gfx950) library for Pulsar Attention's
+ * Phase-1 statistical context encoding and Phase-2 query attention.
+ *
+ * Paper: "Dropping the Anchor: Statistical Context Summarization for
+ * Distributed Systems via Pulsar Attention" (arXiv 2607.20457).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument is a device pointer (memory from hipMalloc or a
+ *   PyTorch CUDA/HIP tensor) unless stated otherwise.  The caller owns all
+ *   buffers; the library allocates no device memory.
+ * - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *   Every call is asynchronous on that stream.  The return value reports
+ *   host-side argument validation and launch errors only; a fault during
+ *   execution surfaces at the caller's next synchronisation.
+ * - Tensors are dense and row-major.  Per-token tensors are laid out
+ *   [batch, tokens, heads, head_dim].  Element offsets are computed in 64 bits.
+ * - bf16 tensors are passed as raw 16-bit storage (IEEE bfloat16).
+ * - Return codes are pulsar_status values; 0 is success.
+ * - The library keeps no mutable global state; calls on different streams
+ *   may run concurrently as long as their output buffers do not overlap.
+ */
+#ifndef PULSAR_H_
+#define PULSAR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PULSAR_OK = 0,
+  PULSAR_EINVAL = -1,        /* an argument is out of range or a required pointer is NULL */
+  PULSAR_EUNSUPPORTED = -2,  /* valid by the paper's definition but outside what this build runs */
+  PULSAR_EHIP = -3,          /* the HIP runtime reported an error at launch */
+  PULSAR_EWORKSPACE = -4     /* the workspace is NULL or smaller than the size query returned */
+} pulsar_status;
+
+typedef enum {
+  /* Input_i = [S_sink || Sigma_0 || ... || Sigma_{i-1} || B_i] (Eq. 3) */
+  PULSAR_PREFIX_SUMMARY = 0,
+  /* Star Attention anchor baseline: Input_i = [B_0 || B_i] (Section 2) */
+  PULSAR_PREFIX_ANCHOR = 1
+} pulsar_prefix_mode;
+
+typedef enum { PULSAR_OUT_F32 = 0, PULSAR_OUT_BF16 = 1 } pulsar_out_dtype;
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* pulsar_status_string(int status);
+
+/* Library ABI version (increases on any signature change). */
+int pulsar_version(void);
+
+/*
+ * Max-IDF summaries (Section 3.1 "Summary generation", Eq. 2; Appendix
+ * "Corpus-Level IDF Table", Eq. idf, and "Max-IDF", Eq. maxidf; the summary
+ * step of Algorithm 1).
+ *
+ * For each of `batch` sequences of `L` token ids, split into `num_blocks`
+ * contiguous blocks of Lb = L / num_blocks tokens:
+ *   df(t)   = number of blocks of that sequence containing t;
+ *   IDF(t)  = ln(num_blocks / max(df(t), 1));
+ *   each block is cut into Lb / chunk non-overlapping chunks of `chunk`
+ *   tokens; a chunk's score is the largest IDF among its tokens;
+ *   the `topk` best chunks of each block (best = higher score, then lower
+ *   chunk index) are written in ascending chunk-index order.
+ * Ranking uses the per-chunk minimum df, which orders chunks exactly as the
+ * maximum IDF does because the logarithm is strictly decreasing.
+ *
+ * ids         int32 [batch, L], each in [0, vocab); 16-byte aligned.
+ *             Ids outside that range are the caller's error: they are
+ *             skipped (no memory fault) and the result is unspecified.
+ * sel_chunks  out int32 [batch, num_blocks, topk], chunk indices within the
+ *             block, ascending.
+ * chunk_mindf out int32 [batch, num_blocks, Lb / chunk], nullable: the
+ *             minimum df of each chunk (IDF of the chunk score = ln(N/mindf)).
+ * idf         out float [batch, vocab], nullable: IDF(t) for every id.
+ *
+ * EINVAL: batch < 0, L < 0, num_blocks < 1, L % num_blocks != 0,
+ *         Lb % chunk != 0, chunk < 1, topk < 0 or topk > Lb / chunk,
+ *         vocab < 1, a NULL ids/sel_chunks pointer when batch*L > 0 (resp.
+ *         batch*num_blocks*topk > 0), misaligned ids.
+ * EUNSUPPORTED: num_blocks > 255, chunk not a power of two in [4, 256],
+ *         or vocab/L/chunk such that the per-sequence df table and chunk
+ *         scores do not fit in one compute unit's 160 KB local data share
+ *         (vocab up to about 145,000 at chunk 32 and L = 128K).
+ */
+int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks,
+                            int chunk, int topk, int vocab, int32_t* sel_chunks,
+                            int32_t* chunk_mindf, float* idf, void* stream);
+
+/*
+ * Number of rows n_i of block i's Phase-1 input (Eq. 3; Appendix
+ * "Block-to-Host Scalability Analysis"):
+ *   block 0: Lb;  summary mode: Lb + sink + block_idx * topk * chunk;
+ *   anchor mode (block_idx > 0): 2 * Lb.
+ * Returns n_i >= 0, or a negative pulsar_status on invalid arguments
+ * (L % num_blocks != 0, block_idx outside [0, num_blocks), sink > Lb,
+ * topk * chunk > Lb, negative sizes, unknown mode).  Host-only; no GPU call.
+ */
+int64_t pulsar_phase1_len(int64_t L, int num_blocks, int block_idx, int sink, int chunk,
+                          int topk, int prefix_mode);
+
+/*
+ * Row -> global position map of block i's Phase-1 input (Eq. 3 with sparse
+ * position ids, Section 3.1 "Causal Assembly"; Appendix "RoPE Position ID
+ * Assignment").  Rows [0, sink) are positions 0..sink-1; then for every
+ * earlier block j < i and every selected chunk c of Sigma_j (in the order of
+ * sel_chunks) the m positions j*Lb + c*m + r; then block i's own positions
+ * i*Lb + r.  Block 0 is [B_0] alone; anchor mode is [B_0 || B_i].
+ *
+ * sel_chunks  int32 [batch, num_blocks, topk] (as written by
+ *             pulsar_maxidf_summaries); only blocks < block_idx are read;
+ *             may be NULL in anchor mode, when block_idx == 0 or topk == 0.
+ *             Chunk indices must lie in [0, Lb / chunk).
+ * pos         out int32 [batch, n_i].
+ * Errors: as pulsar_phase1_len, plus EINVAL for NULL pointers, batch < 0,
+ *         or L >= 2^31.
+ */
+int pulsar_phase1_positions(const int32_t* sel_chunks, int batch, int64_t L, int num_blocks,
+                            int block_idx, int sink, int chunk, int topk, int prefix_mode,
+                            int32_t* pos, void* stream);
+
+/*
+ * Phase-1 prefixed-block causal attention (Algorithm 1, forward pass of
+ * Input_i; Eq. 1 with an index-causal mask over the assembled rows; KV
+ * discard per Appendix "KV Cache Discard").
+ *
+ * Every row r of Input_i (n_i rows, order of Eq. 3, see
+ * pulsar_phase1_positions) is a query row and attends to rows 0..r of
+ * Input_i.  The query/key/value of a row are those of the token at its
+ * global position; the assembly is fused into the kernel's loads and never
+ * materialised.  Query head h reads KV head h / (Hq / Hkv).
+ *
+ * Q           bf16 [batch, L, Hq, d];  K, V  bf16 [batch, L, Hkv, d].
+ * sel_chunks  int32 [batch, num_blocks, topk]; nullable as for
+ *             pulsar_phase1_positions.
+ * softmax_scale  multiplies q.k (the paper's 1/sqrt(d)).
+ * O           out [batch, n_i, Hq, d], float32 or bf16 per o_dtype.
+ * lse         out float32 [batch, Hq, n_i], nullable: ln sum_c exp(s_rc).
+ * K_keep, V_keep  out bf16 [batch, Lb, Hkv, d], nullable (both or none):
+ *             the retained KV(B_i) rows, i.e. the last Lb rows of Input_i.
+ *
+ * EINVAL: shape/size errors as pulsar_phase1_len, batch < 0, Hq % Hkv != 0,
+ *         NULL Q/K/V/O, softmax_scale not finite and > 0, only one of
+ *         K_keep/V_keep given, L >= 2^31.
+ * EUNSUPPORTED: d not in {64, 128}; Hq / Hkv not 1, 2 or a multiple of 4.
+ */
+int pulsar_phase1_attn(const void* Q, const void* K, const void* V, int batch, int64_t L,
+                       int Hq, int Hkv, int d, int num_blocks, int block_idx, int sink,
+                       int chunk, int topk, const int32_t* sel_chunks, int prefix_mode,
+                       float softmax_scale, void* O, int o_dtype, float* lse, void* K_keep,
+                       void* V_keep, void* stream);
+
+/*
+ * Device workspace, in bytes, that pulsar_phase2_partial needs for these
+ * shapes (0 when none is needed).  Host-only.
+ */
+size_t pulsar_phase2_workspace_bytes(int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d);
+
+/*
+ * Phase-2 per-shard partial attention (Algorithm 1, Phase 2:
+ * (A_h, l_h) <- FlashAttn(q, KV_h) for every host h; Appendix "Phase 2
+ * Distributed Softmax Merge").  One launch computes all n_shards shards, in
+ * place of n_shards hosts.
+ *
+ * For each shard h: o_h = softmax(q K_h^T * scale) V_h and
+ * l_h = ln sum_c exp(q . k_c * scale), with no mask.
+ *
+ * q           bf16 [Tq, Hq, d].
+ * K, V        bf16 [n_shards, S, Hkv, d] (shard h is rows [h*S, (h+1)*S)).
+ * o_parts     out float32 [n_shards, Tq, Hq, d].
+ * lse_parts   out float32 [n_shards, Hq, Tq].
+ * workspace   device buffer of at least pulsar_phase2_workspace_bytes(...)
+ *             bytes (may be NULL when that is 0).  Its contents on entry
+ *             do not matter.
+ * An empty shard (S == 0) gives lse = -inf and o = 0.
+ *
+ * EINVAL: negative sizes, Hq % Hkv != 0, NULL required pointers, scale not
+ *         finite and > 0.  EWORKSPACE: workspace too small.
+ * EUNSUPPORTED: d not in {64, 128}; Hq / Hkv not 1, 2 or a multiple of 4.
+ */
+int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_shards, int Tq,
+                          int64_t S, int Hq, int Hkv, int d, float softmax_scale,
+                          float* o_parts, float* lse_parts, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/*
+ * Online-softmax merge of H partials (Algorithm 1, Phase 2 merge; Appendix
+ * "Phase 2 Distributed Softmax Merge", Eqs. lse-merge and out-merge).
+ * Produces l = ln sum_h exp(l_h) and o = sum_h exp(l_h - l) o_h, which is
+ * what folding Eq. lse-merge / Eq. out-merge over h gives in exact
+ * arithmetic; partials with l_h = -inf contribute nothing, and if every
+ * l_h is -inf the result is l = -inf, o = 0.
+ *
+ * o_parts     float32 [H, Tq, Hq, d];  lse_parts float32 [H, Hq, Tq].
+ * o           out float32 [Tq, Hq, d]; lse out float32 [Hq, Tq] (nullable).
+ * EINVAL: H < 1, negative sizes, NULL required pointers, d % 4 != 0.
+ */
+int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq, int Hq,
+                     int d, float* o, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PULSAR_H_ */

@@ -1,0 +1,9 @@
+"""Pulsar Attention Phase-1 / Phase-2 hot path for MI355X (gfx950).
+
+The computation lives in ``libpulsar.so`` (HIP kernels behind the C ABI of
+``include/pulsar.h``); ``api`` is its thin torch-facing binding and
+``workload`` draws the seeded synthetic inputs.
+"""
+from .api import (OUT_BF16, OUT_F32, PREFIX_ANCHOR, PREFIX_SUMMARY, lse_merge,  # noqa: F401
+                  maxidf_summaries, phase1_attn, phase1_len, phase1_positions, phase2_partial,
+                  phase2_workspace_bytes)

@@ -1,0 +1,272 @@
+// C ABI entry points: host-side validation, then kernel launches.
+#include <math.h>
+
+#include "common.hpp"
+
+namespace {
+
+constexpr int kVersion = 1;
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// Shape checks shared by the Phase-1 calls (Eq. 3 row counts).
+int64_t phase1_len_checked(int64_t L, int num_blocks, int block_idx, int sink, int chunk, int topk,
+                           int prefix_mode) {
+  if (L < 0 || num_blocks < 1 || L % num_blocks != 0) return PULSAR_EINVAL;
+  if (block_idx < 0 || block_idx >= num_blocks) return PULSAR_EINVAL;
+  if (prefix_mode != PULSAR_PREFIX_SUMMARY && prefix_mode != PULSAR_PREFIX_ANCHOR)
+    return PULSAR_EINVAL;
+  const int64_t Lb = L / num_blocks;
+  if (sink < 0 || sink > Lb) return PULSAR_EINVAL;
+  if (chunk < 1 || topk < 0 || (int64_t)topk * chunk > Lb) return PULSAR_EINVAL;
+  if (block_idx == 0) return Lb;
+  if (prefix_mode == PULSAR_PREFIX_ANCHOR) return 2 * Lb;
+  return Lb + sink + (int64_t)block_idx * topk * chunk;
+}
+
+RowMap make_map(int64_t L, int num_blocks, int block_idx, int sink, int chunk, int topk,
+                int prefix_mode) {
+  RowMap mp{};
+  const int Lb = (int)(L / num_blocks);
+  mp.block_idx = block_idx;
+  mp.Lb = Lb;
+  mp.sink = sink;
+  mp.chunk = chunk;
+  mp.topk = topk;
+  mp.sigma = topk * chunk;
+  mp.inv_sigma = mp.sigma > 0 ? 1.0f / (float)mp.sigma : 0.f;
+  mp.inv_chunk = 1.0f / (float)chunk;
+  mp.nchunk = Lb / chunk;
+  if (block_idx == 0) {
+    mp.mode = MAP_IDENTITY;
+    mp.offset = 0;
+  } else if (prefix_mode == PULSAR_PREFIX_ANCHOR) {
+    mp.mode = MAP_ANCHOR;
+  } else if (topk == 0) {
+    mp.mode = MAP_SUMMARY;
+    mp.prefix = 0;
+  } else {
+    mp.mode = MAP_SUMMARY;
+    mp.prefix = block_idx * mp.sigma;
+  }
+  return mp;
+}
+
+bool needs_sel(int block_idx, int topk, int prefix_mode) {
+  return block_idx > 0 && topk > 0 && prefix_mode == PULSAR_PREFIX_SUMMARY;
+}
+
+bool heads_supported(int Hq, int Hkv) {
+  const int group = Hq / Hkv;
+  return group == 1 || group == 2 || group % 4 == 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pulsar_status_string(int status) {
+  switch (status) {
+    case PULSAR_OK: return "ok";
+    case PULSAR_EINVAL: return "invalid argument";
+    case PULSAR_EUNSUPPORTED: return "unsupported configuration";
+    case PULSAR_EHIP: return "HIP runtime error";
+    case PULSAR_EWORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+  }
+}
+
+int pulsar_version(void) { return kVersion; }
+
+int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                            int topk, int vocab, int32_t* sel_chunks, int32_t* chunk_mindf,
+                            float* idf, void* stream) {
+  if (batch < 0 || L < 0 || num_blocks < 1 || vocab < 1 || chunk < 1 || topk < 0)
+    return PULSAR_EINVAL;
+  if (L % num_blocks != 0) return PULSAR_EINVAL;
+  const int64_t Lb = L / num_blocks;
+  if (Lb % chunk != 0 || topk > Lb / chunk) return PULSAR_EINVAL;
+  if ((int64_t)batch * L > 0 && (ids == nullptr || !aligned16(ids))) return PULSAR_EINVAL;
+  if ((int64_t)batch * num_blocks * topk > 0 && sel_chunks == nullptr) return PULSAR_EINVAL;
+  if (num_blocks > 255 || !is_pow2(chunk) || chunk < 4 || chunk > 256) return PULSAR_EUNSUPPORTED;
+  if (L >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
+  const size_t lds = maxidf_lds_bytes(L, chunk, vocab);
+  if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
+  return launch_maxidf(ids, batch, L, num_blocks, chunk, topk, vocab, sel_chunks, chunk_mindf, idf,
+                       lds, (hipStream_t)stream);
+}
+
+int64_t pulsar_phase1_len(int64_t L, int num_blocks, int block_idx, int sink, int chunk, int topk,
+                          int prefix_mode) {
+  return phase1_len_checked(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+}
+
+int pulsar_phase1_positions(const int32_t* sel_chunks, int batch, int64_t L, int num_blocks,
+                            int block_idx, int sink, int chunk, int topk, int prefix_mode,
+                            int32_t* pos, void* stream) {
+  const int64_t n = phase1_len_checked(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  if (n < 0) return (int)n;
+  if (batch < 0 || L >= ((int64_t)1 << 31)) return PULSAR_EINVAL;
+  if (batch == 0 || n == 0) return PULSAR_OK;
+  if (pos == nullptr) return PULSAR_EINVAL;
+  if (needs_sel(block_idx, topk, prefix_mode) && sel_chunks == nullptr) return PULSAR_EINVAL;
+  const RowMap mp = make_map(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  const int32_t* sel = needs_sel(block_idx, topk, prefix_mode) ? sel_chunks : nullptr;
+  return launch_positions(mp, sel, (int64_t)num_blocks * topk, batch, (int)n, pos,
+                          (hipStream_t)stream);
+}
+
+int pulsar_phase1_attn(const void* Q, const void* K, const void* V, int batch, int64_t L, int Hq,
+                       int Hkv, int d, int num_blocks, int block_idx, int sink, int chunk,
+                       int topk, const int32_t* sel_chunks, int prefix_mode, float softmax_scale,
+                       void* O, int o_dtype, float* lse, void* K_keep, void* V_keep,
+                       void* stream) {
+  const int64_t n = phase1_len_checked(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  if (n < 0) return (int)n;
+  if (batch < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1) return PULSAR_EINVAL;
+  if (L >= ((int64_t)1 << 31)) return PULSAR_EINVAL;
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale)) return PULSAR_EINVAL;
+  if (o_dtype != PULSAR_OUT_F32 && o_dtype != PULSAR_OUT_BF16) return PULSAR_EINVAL;
+  if ((K_keep == nullptr) != (V_keep == nullptr)) return PULSAR_EINVAL;
+  if (d != 64 && d != 128) return PULSAR_EUNSUPPORTED;
+  if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
+  if (batch == 0 || n == 0) return PULSAR_OK;
+  if (Q == nullptr || K == nullptr || V == nullptr || O == nullptr) return PULSAR_EINVAL;
+  if (needs_sel(block_idx, topk, prefix_mode) && sel_chunks == nullptr) return PULSAR_EINVAL;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return PULSAR_EINVAL;
+  if (K_keep != nullptr && (!aligned16(K_keep) || !aligned16(V_keep))) return PULSAR_EINVAL;
+
+  AttnLaunch a{};
+  a.Q = static_cast<const uint16_t*>(Q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  a.q_zstride = L * Hq * d;
+  a.kv_zstride = L * Hkv * d;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.d = d;
+  a.n_q = (int)n;
+  a.n_kv = (int)n;
+  a.causal = 1;
+  a.nsplit = 1;
+  a.split_len = (int)n;
+  a.nz_kv = batch;
+  a.map = make_map(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  a.sel = needs_sel(block_idx, topk, prefix_mode) ? sel_chunks : nullptr;
+  a.sel_bstride = (int64_t)num_blocks * topk;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.O = O;
+  a.o_bf16 = o_dtype == PULSAR_OUT_BF16;
+  a.o_zstride = n * Hq * d;
+  a.lse = lse;
+  a.lse_zstride = (int64_t)Hq * n;
+  int st = launch_attention(a, (hipStream_t)stream);
+  if (st != PULSAR_OK || K_keep == nullptr) return st;
+
+  // KV(B_i): the last Lb rows of Input_i are block i's own tokens.
+  const int64_t Lb = L / num_blocks;
+  const int64_t row_bytes = Lb * Hkv * d * 2;
+  const int64_t src_off = (int64_t)block_idx * Lb * Hkv * d;
+  const int64_t pitch = L * Hkv * d * 2;
+  st = launch_copy_rows(static_cast<const uint16_t*>(K) + src_off, pitch, K_keep, row_bytes,
+                        row_bytes, batch, (hipStream_t)stream);
+  if (st != PULSAR_OK) return st;
+  return launch_copy_rows(static_cast<const uint16_t*>(V) + src_off, pitch, V_keep, row_bytes,
+                          row_bytes, batch, (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+// Phase-2 key splitting: each shard is cut into nsplit ranges so that the
+// launch has enough workgroups to cover the chip; the partials of a shard are
+// then merged with the same online-softmax merge as the shards themselves.
+static int phase2_splits(int n_shards, int Tq, int64_t S, int Hq, int Hkv) {
+  if (S <= 0) return 1;
+  const int group = Hq / Hkv;
+  const int heads_per_wg = group >= 4 ? 4 : group;
+  const int rows_per_wg = 32 * (4 / heads_per_wg);
+  const int64_t row_tiles = (Tq + rows_per_wg - 1) / rows_per_wg;
+  const int64_t base = row_tiles * (group / heads_per_wg) * Hkv * n_shards;
+  const int64_t target = 2048;  // about 8 workgroups per compute unit
+  int64_t ns = (target + base - 1) / base;
+  const int64_t max_by_len = (S + 511) / 512;  // keep at least 512 keys per split
+  if (ns > max_by_len) ns = max_by_len;
+  if (ns < 1) ns = 1;
+  if (ns > 64) ns = 64;
+  return (int)ns;
+}
+
+extern "C" {
+
+size_t pulsar_phase2_workspace_bytes(int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d) {
+  if (n_shards < 0 || Tq < 0 || S < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1) return 0;
+  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv);
+  if (ns <= 1) return 0;
+  const int64_t per = (int64_t)n_shards * ns;
+  return (size_t)(per * Tq * Hq * d * 4 + per * Hq * Tq * 4);
+}
+
+int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_shards, int Tq,
+                          int64_t S, int Hq, int Hkv, int d, float softmax_scale, float* o_parts,
+                          float* lse_parts, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  if (n_shards < 0 || Tq < 0 || S < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1)
+    return PULSAR_EINVAL;
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale)) return PULSAR_EINVAL;
+  if (d != 64 && d != 128) return PULSAR_EUNSUPPORTED;
+  if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
+  if (S >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
+  if (n_shards == 0 || Tq == 0) return PULSAR_OK;
+  if (q == nullptr || o_parts == nullptr || lse_parts == nullptr) return PULSAR_EINVAL;
+  if (S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;
+  if (!aligned16(q) || (S > 0 && (!aligned16(K) || !aligned16(V))) || !aligned16(o_parts))
+    return PULSAR_EINVAL;
+  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv);
+  const size_t need = pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
+    return PULSAR_EWORKSPACE;
+
+  AttnLaunch a{};
+  a.Q = static_cast<const uint16_t*>(q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  a.q_zstride = 0;
+  a.kv_zstride = S * Hkv * d;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.d = d;
+  a.n_q = Tq;
+  a.n_kv = (int)S;
+  a.causal = 0;
+  a.nsplit = ns;
+  a.split_len = (int)((S + ns - 1) / ns);
+  a.nz_kv = n_shards;
+  a.map = RowMap{};
+  a.map.mode = MAP_IDENTITY;
+  a.sel = nullptr;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.o_bf16 = 0;
+  a.o_zstride = (int64_t)Tq * Hq * d;
+  a.lse_zstride = (int64_t)Hq * Tq;
+  float* ws_o = static_cast<float*>(workspace);
+  float* ws_l = ws_o + (int64_t)n_shards * ns * Tq * Hq * d;
+  a.O = ns > 1 ? ws_o : o_parts;
+  a.lse = ns > 1 ? ws_l : lse_parts;
+  int st = launch_attention(a, (hipStream_t)stream);
+  if (st != PULSAR_OK || ns == 1) return st;
+  return launch_lse_merge(ws_o, ws_l, ns, n_shards, Tq, Hq, d, (int64_t)Tq * Hq * d,
+                          (int64_t)Hq * Tq, o_parts, lse_parts, (hipStream_t)stream);
+}
+
+int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq, int Hq, int d,
+                     float* o, float* lse, void* stream) {
+  if (H < 1 || Tq < 0 || Hq < 0 || d < 1 || d % 4 != 0) return PULSAR_EINVAL;
+  if ((int64_t)Tq * Hq == 0) return PULSAR_OK;
+  if (o_parts == nullptr || lse_parts == nullptr || o == nullptr) return PULSAR_EINVAL;
+  if (!aligned16(o_parts) || !aligned16(o)) return PULSAR_EINVAL;
+  return launch_lse_merge(o_parts, lse_parts, H, 1, Tq, Hq, d, (int64_t)Tq * Hq * d,
+                          (int64_t)Hq * Tq, o, lse, (hipStream_t)stream);
+}
+
+}  // extern "C"

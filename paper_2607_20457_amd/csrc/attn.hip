@@ -1,0 +1,367 @@
+// Flash-style attention on gfx950 bf16 matrix cores, shared by
+//  * Phase 1: index-causal attention over block i's assembled input
+//    [S_sink || Sigma_0..Sigma_{i-1} || B_i] (Eq. 3, Eq. 1), whose rows are
+//    gathered from the global Q/K/V through the row -> position map, and
+//  * Phase 2: unmasked attention of the query over each retained KV shard,
+//    split along the keys, giving (o, lse) partials (Algorithm 1, Phase 2).
+//
+// Work decomposition
+//   A workgroup is 4 wavefronts.  All of them read the same KV head; when the
+//   group size Hq/Hkv is a multiple of 4 the waves are 4 query heads of that
+//   group over the same 32*QT rows (grouped-query sharing: one K/V tile in
+//   LDS feeds four heads), otherwise the waves also split the rows.
+//   Workgroup ids run heaviest causal row tile first, and the KV head is the
+//   fastest-varying index, so with 8 KV heads each XCD's L2 serves one head.
+//
+// Per wavefront, per 64-key tile (32x32x16 bf16 MFMA, fp32 accumulate)
+//   S^T = K Q^T   A = K rows from LDS, B = Q fragments held in registers;
+//                 the lane of query q holds 16 scores of q per 32-key block.
+//   online softmax in the log2 domain on those registers; the running max is
+//                 only raised when it grows by more than 2^8 (the final
+//                 normalisation divides by a sum taken with the same max, so
+//                 the result is unchanged and the O rescale is rare).
+//   O^T += V^T P^T  A = V^T from LDS (V is transposed on its way into LDS),
+//                 B = P, which is already in the B-operand layout because K
+//                 rows are stored in LDS with bits 2 and 3 of the key index
+//                 swapped.
+//   K/V tiles are double-buffered: the next tile's global loads are issued
+//   before the current tile's math and written to LDS after it.
+#include "common.hpp"
+
+namespace {
+
+constexpr int BN = 64;          // keys per tile
+constexpr int THREADS = 256;    // 4 wavefronts
+constexpr float MAX_SLACK = 8.0f;  // log2-domain slack before the running max is raised
+
+template <int D>
+struct Tile {
+  static constexpr int K_STRIDE = D * 2 + 16;   // bytes per K row in LDS (padded)
+  static constexpr int V_STRIDE = BN * 2 + 16;  // bytes per V^T row (one head_dim entry)
+  static constexpr int K_BYTES = BN * K_STRIDE;
+  static constexpr int V_BYTES = D * V_STRIDE;
+  static constexpr int STAGE = K_BYTES + V_BYTES;
+  static constexpr int LDS = 2 * STAGE + 2 * BN * 4;  // two stages + two position rows
+  static constexpr int CPR = D / 8;               // 16-byte chunks per row
+  static constexpr int K_ROWS_PER_PASS = THREADS / CPR;
+  static constexpr int K_PASSES = BN / K_ROWS_PER_PASS;
+  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit
+  static constexpr int V_PASSES = (V_UNITS + THREADS - 1) / THREADS;
+};
+
+struct KernelArgs {
+  AttnLaunch a;
+  int group;          // Hq / Hkv
+  int heads_per_wg;   // query heads per workgroup (1, 2 or 4)
+  int hsub;           // workgroups per KV head along the head axis
+  int rows_per_wg;    // query rows per workgroup
+  int n_row_tiles;
+  int nz;             // z extent (sequences, or shards x splits)
+};
+
+__device__ __forceinline__ int swap_bits23(int r) {
+  return (r & ~12) | ((r >> 1) & 4) | ((r << 1) & 8);
+}
+
+__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
+  return (a & 0xFFFFu) | (b << 16);
+}
+__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
+  return (a >> 16) | (b & 0xFFFF0000u);
+}
+
+template <int D, int QT, bool CAUSAL>
+__global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
+  using T = Tile<D>;
+  constexpr int QR = 32 * QT;        // rows per wavefront
+  constexpr int DS = D / 16;         // k-steps of the S product
+  constexpr int DT = D / 32;         // 32-row tiles of O^T
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const AttnLaunch& a = ka.a;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l32 = lane & 31;
+  const int g = lane >> 5;
+
+  // ---- workgroup -> (kv head, head slice, z, row tile) ---------------------
+  int bid = blockIdx.x;
+  const int kvh = bid % a.Hkv;
+  bid /= a.Hkv;
+  const int hs = bid % ka.hsub;
+  bid /= ka.hsub;
+  const int z = bid % ka.nz;
+  bid /= ka.nz;
+  const int row_tile = ka.n_row_tiles - 1 - bid;
+
+  const int head = kvh * ka.group + hs * ka.heads_per_wg + (wave % ka.heads_per_wg);
+  const int wg_row0 = row_tile * ka.rows_per_wg;
+  const int row0 = wg_row0 + (wave / ka.heads_per_wg) * QR;
+
+  const int zkv = z / a.nsplit;
+  const int split = z - zkv * a.nsplit;
+  const int kv_begin = split * a.split_len;
+  int kv_end = min(a.n_kv, kv_begin + a.split_len);
+  if (CAUSAL) kv_end = min(kv_end, wg_row0 + ka.rows_per_wg);
+  const int n_keys = max(0, kv_end - kv_begin);
+  const int ntiles = (n_keys + BN - 1) / BN;
+
+  const int32_t* sel = a.sel ? a.sel + zkv * a.sel_bstride : nullptr;
+  const int64_t q_row = (int64_t)a.Hq * D;
+  const int64_t kv_row = (int64_t)a.Hkv * D;
+  const uint16_t* Qz = a.Q + zkv * a.q_zstride + (int64_t)head * D;
+  const uint16_t* Kz = a.K + zkv * a.kv_zstride + (int64_t)kvh * D;
+  const uint16_t* Vz = a.V + zkv * a.kv_zstride + (int64_t)kvh * D;
+
+  uint8_t* stage0 = smem;
+  int32_t* lpos = reinterpret_cast<int32_t*>(smem + 2 * T::STAGE);  // [2][BN]
+
+  // ---- Q fragments (B operand of S^T = K Q^T) --------------------------------
+  bf16x8 qf[QT][DS];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int r = row0 + t * 32 + l32;
+    if (r < a.n_q) {
+      const int p = row_position(a.map, sel, r);
+      const bf16x8* src = reinterpret_cast<const bf16x8*>(Qz + (int64_t)p * q_row) + g;
+#pragma unroll
+      for (int s = 0; s < DS; ++s) qf[t][s] = src[2 * s];
+    } else {
+#pragma unroll
+      for (int s = 0; s < DS; ++s) qf[t][s] = bf16x8{};
+    }
+  }
+
+  f32x16 acc[DT][QT];
+#pragma unroll
+  for (int e = 0; e < DT; ++e)
+#pragma unroll
+    for (int t = 0; t < QT; ++t) acc[e][t] = f32x16{};
+  float m_run[QT], l_run[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+  }
+
+  // ---- cooperative tile loads -----------------------------------------------
+  auto tile_positions = [&](int j, int32_t* dst) {
+    if (tid < BN) {
+      const int k = kv_begin + j * BN + tid;
+      dst[tid] = k < kv_end ? row_position(a.map, sel, k) : -1;
+    }
+  };
+  u32x4 kreg[T::K_PASSES];
+  u32x4 vreg[T::V_PASSES][4];
+  auto load_regs = [&](const int32_t* pos) {
+#pragma unroll
+    for (int it = 0; it < T::K_PASSES; ++it) {
+      const int r = it * T::K_ROWS_PER_PASS + tid / T::CPR;
+      const int p = pos[r];
+      kreg[it] = p >= 0 ? *reinterpret_cast<const u32x4*>(Kz + (int64_t)p * kv_row +
+                                                           (tid % T::CPR) * 8)
+                        : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int it = 0; it < T::V_PASSES; ++it) {
+      const int u = tid + it * THREADS;
+      if (u < T::V_UNITS) {
+        const int kq = u & 15;
+        const int dc = u >> 4;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int p = pos[4 * kq + rr];
+          vreg[it][rr] = p >= 0 ? *reinterpret_cast<const u32x4*>(Vz + (int64_t)p * kv_row + dc * 8)
+                                : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+    }
+  };
+  auto store_lds = [&](uint8_t* st) {
+#pragma unroll
+    for (int it = 0; it < T::K_PASSES; ++it) {
+      const int r = it * T::K_ROWS_PER_PASS + tid / T::CPR;
+      *reinterpret_cast<u32x4*>(st + swap_bits23(r) * T::K_STRIDE + (tid % T::CPR) * 16) = kreg[it];
+    }
+    uint8_t* sv = st + T::K_BYTES;
+#pragma unroll
+    for (int it = 0; it < T::V_PASSES; ++it) {
+      const int u = tid + it * THREADS;
+      if (u < T::V_UNITS) {
+        const int kq = u & 15;
+        const int dc = u >> 4;
+        const u32x4* r4 = vreg[it];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
+          const u32x2 lo = {pack_lo(r4[0][w], r4[1][w]), pack_lo(r4[2][w], r4[3][w])};
+          const u32x2 hi = {pack_hi(r4[0][w], r4[1][w]), pack_hi(r4[2][w], r4[3][w])};
+          *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
+          *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
+        }
+      }
+    }
+  };
+
+  if (ntiles > 0) {
+    tile_positions(0, lpos);
+    __syncthreads();
+    if (ntiles > 1) tile_positions(1, lpos + BN);
+    load_regs(lpos);
+    store_lds(stage0);
+  }
+
+  // ---- main loop over key tiles ---------------------------------------------
+  for (int j = 0; j < ntiles; ++j) {
+    __syncthreads();
+    const int buf = j & 1;
+    if (j + 1 < ntiles) load_regs(lpos + ((j + 1) & 1) * BN);
+    if (j + 2 < ntiles) tile_positions(j + 2, lpos + buf * BN);
+
+    const int kbase = kv_begin + j * BN;
+    const bool wave_active = !CAUSAL || kbase <= row0 + QR - 1;
+    if (wave_active) {
+      const uint8_t* sK = stage0 + buf * T::STAGE;
+      const uint8_t* sV = sK + T::K_BYTES;
+
+      f32x16 S[2][QT];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+#pragma unroll
+        for (int t = 0; t < QT; ++t) S[u][t] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
+                                                             (16 * s + 8 * g) * 2);
+#pragma unroll
+          for (int t = 0; t < QT; ++t)
+            S[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[u][t], 0, 0, 0);
+        }
+      }
+
+      const bool edge = CAUSAL ? (kbase + BN - 1 > row0) : (kbase + BN > kv_end);
+      bf16x8 pf[2][2][QT];
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        if (edge) {
+          const int qrow = row0 + t * 32 + l32;
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int key = kbase + u * 32 + 16 * (v >> 3) + 8 * g + (v & 7);
+              const bool masked = CAUSAL ? (key > qrow || key >= kv_end) : (key >= kv_end);
+              if (masked) S[u][t][v] = -INFINITY;
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, S[u][t][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = mx * a.scale_log2;
+        const bool raise = m_new > m_run[t] + MAX_SLACK;
+        const float m_use = raise ? m_new : m_run[t];
+        if (__any(raise)) {
+          const float alpha = exp2f(m_run[t] - m_use);
+#pragma unroll
+          for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
+          l_run[t] *= alpha;
+        }
+        m_run[t] = m_use;
+        float psum = 0.f;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            f32x8 p;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+              p[v] = exp2f(__builtin_fmaf(S[u][t][8 * c + v], a.scale_log2, -m_use));
+              psum += p[v];
+            }
+            pf[u][c][t] = __builtin_convertvector(p, bf16x8);
+          }
+        l_run[t] += psum;
+      }
+
+#pragma unroll
+      for (int e = 0; e < DT; ++e)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+                sV + (e * 32 + l32) * T::V_STRIDE + (u * 32 + 16 * c + 8 * g) * 2);
+#pragma unroll
+            for (int t = 0; t < QT; ++t)
+              acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u][c][t], acc[e][t], 0, 0, 0);
+          }
+    }
+
+    if (j + 1 < ntiles) store_lds(stage0 + (buf ^ 1) * T::STAGE);
+  }
+
+  // ---- epilogue: normalise, write O and LSE ---------------------------------
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const float l_tot = l_run[t] + __shfl_xor(l_run[t], 32, 64);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const int qrow = row0 + t * 32 + l32;
+    if (qrow < a.n_q) {
+      const int64_t obase = ((int64_t)z * a.o_zstride) + ((int64_t)qrow * a.Hq + head) * D;
+#pragma unroll
+      for (int e = 0; e < DT; ++e)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int dd = e * 32 + 8 * q4 + 4 * g;
+          f32x4 o4 = {acc[e][t][4 * q4] * inv, acc[e][t][4 * q4 + 1] * inv,
+                      acc[e][t][4 * q4 + 2] * inv, acc[e][t][4 * q4 + 3] * inv};
+          if (a.o_bf16) {
+            *reinterpret_cast<bf16x4*>(reinterpret_cast<uint16_t*>(a.O) + obase + dd) =
+                __builtin_convertvector(o4, bf16x4);
+          } else {
+            *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.O) + obase + dd) = o4;
+          }
+        }
+      if (a.lse && g == 0) {
+        const float lse = l_tot > 0.f ? (m_run[t] + __log2f(l_tot)) * 0.69314718055994531f
+                                      : -INFINITY;
+        a.lse[(int64_t)z * a.lse_zstride + (int64_t)head * a.n_q + qrow] = lse;
+      }
+    }
+  }
+}
+
+template <int D, int QT, bool CAUSAL>
+int launch_impl(const KernelArgs& ka, hipStream_t stream) {
+  const int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
+  if (nwg == 0) return PULSAR_OK;
+  if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
+  auto kern = attn_fwd_kernel<D, QT, CAUSAL>;
+  if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          Tile<D>::LDS) != hipSuccess)
+    return PULSAR_EHIP;
+  hipLaunchKernelGGL(kern, dim3((unsigned)nwg), dim3(THREADS), Tile<D>::LDS, stream, ka);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+}  // namespace
+
+int launch_attention(const AttnLaunch& a, hipStream_t stream) {
+  KernelArgs ka;
+  ka.a = a;
+  ka.group = a.Hq / a.Hkv;
+  ka.heads_per_wg = ka.group >= 4 ? 4 : ka.group;
+  ka.hsub = ka.group / ka.heads_per_wg;
+  constexpr int QT = 1;
+  ka.rows_per_wg = 32 * QT * (4 / ka.heads_per_wg);
+  ka.n_row_tiles = (a.n_q + ka.rows_per_wg - 1) / ka.rows_per_wg;
+  ka.nz = a.nz_kv * a.nsplit;
+  if (a.d == 128) {
+    return a.causal ? launch_impl<128, QT, true>(ka, stream) : launch_impl<128, QT, false>(ka, stream);
+  }
+  return a.causal ? launch_impl<64, QT, true>(ka, stream) : launch_impl<64, QT, false>(ka, stream);
+}

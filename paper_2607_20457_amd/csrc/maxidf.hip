@@ -1,0 +1,192 @@
+// Max-IDF summary construction on gfx950 (Section 3.1 "Summary generation",
+// Eq. 2; Appendix "Corpus-Level IDF Table" and "Max-IDF").
+//
+// One 1024-thread workgroup per sequence keeps the whole document-frequency
+// table of that sequence in the compute unit's local data share (LDS), so the
+// table never touches HBM:
+//
+//   pass 1  for every block j: clear a vocab-sized bitmap, stream the block's
+//           ids with 16-byte loads, atomically set each id's bit; the thread
+//           that sets a bit first adds one to that id's df byte (df <= 255).
+//   pass 2  stream the ids again; each lane looks up the df of its four ids,
+//           and lanes of one chunk (chunk/4 lanes) take the minimum with
+//           cross-lane shuffles.  The chunk minima go to LDS (and optionally
+//           to HBM).
+//   select  one wavefront per block finds the threshold tau, the smallest df
+//           with at least k chunks at or below it (binary search over
+//           1..N with wave-wide counts), keeps every chunk below tau and the
+//           first k - #(< tau) chunks equal to tau in index order, and writes
+//           the kept indices in ascending order with a wave prefix sum.
+//
+// A chunk's Max-IDF score ln(N / mindf) is strictly decreasing in mindf, so
+// ranking by (mindf ascending, index ascending) is ranking by (score
+// descending, index ascending).
+#include "common.hpp"
+
+#define MAXIDF_THREADS 1024
+#define MAXIDF_WAVES (MAXIDF_THREADS / PULSAR_WAVE)
+
+static inline int64_t round_up4(int64_t x) { return (x + 3) & ~int64_t(3); }
+
+// LDS layout: df bytes [round_up4(vocab)], then a region reused as the
+// per-block bitmap (pass 1) and the chunk minima (pass 2 / select).
+size_t maxidf_lds_bytes(int64_t L, int chunk, int vocab) {
+  int64_t df_bytes = round_up4(vocab);
+  int64_t bitmap_bytes = ((int64_t)vocab + 31) / 32 * 4;
+  int64_t chunk_bytes = round_up4(L / chunk);
+  return (size_t)(df_bytes + (bitmap_bytes > chunk_bytes ? bitmap_bytes : chunk_bytes));
+}
+
+__device__ __forceinline__ void mark_token(int t, int vocab, uint32_t* bits, uint32_t* dfw) {
+  if ((unsigned)t >= (unsigned)vocab) return;  // caller error: skipped, never out of bounds
+  const uint32_t bit = 1u << (t & 31);
+  const uint32_t old = atomicOr(&bits[t >> 5], bit);
+  if (!(old & bit)) atomicAdd(&dfw[t >> 2], 1u << ((t & 3) * 8));
+}
+
+__device__ __forceinline__ uint32_t df_of(int t, int vocab, const uint8_t* df8) {
+  return (unsigned)t < (unsigned)vocab ? (uint32_t)df8[t] : 255u;
+}
+
+__global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
+    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2,
+    int topk, int vocab, int32_t* __restrict__ sel, int32_t* __restrict__ chunk_mindf,
+    float* __restrict__ idf) {
+  extern __shared__ uint32_t lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t b = blockIdx.x;
+  const int chunk = 1 << chunk_log2;
+  const int vocab_w4 = (vocab + 3) >> 2;
+  const int vocab_w32 = (vocab + 31) >> 5;
+  uint32_t* dfw = lds;
+  uint8_t* df8 = reinterpret_cast<uint8_t*>(lds);
+  uint32_t* bits = lds + vocab_w4;
+  uint8_t* cmin = reinterpret_cast<uint8_t*>(bits);
+
+  const int32_t* seq = ids + b * L;
+
+  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = 0u;
+
+  // ---- pass 1: document frequency --------------------------------------
+  const int nvec = Lb >> 2;  // int4 groups per block
+  for (int j = 0; j < num_blocks; ++j) {
+    for (int w = tid; w < vocab_w32; w += MAXIDF_THREADS) bits[w] = 0u;
+    __syncthreads();
+    const int4* blk = reinterpret_cast<const int4*>(seq + (int64_t)j * Lb);
+    for (int v0 = 0; v0 < nvec; v0 += 4 * MAXIDF_THREADS) {
+      int4 t4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v = v0 + u * MAXIDF_THREADS + tid;
+        t4[u] = v < nvec ? blk[v] : make_int4(-1, -1, -1, -1);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        mark_token(t4[u].x, vocab, bits, dfw);
+        mark_token(t4[u].y, vocab, bits, dfw);
+        mark_token(t4[u].z, vocab, bits, dfw);
+        mark_token(t4[u].w, vocab, bits, dfw);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- optional IDF table (Eq. idf) -------------------------------------
+  if (idf) {
+    const float n = (float)num_blocks;
+    float* out = idf + b * vocab;
+    for (int t = tid; t < vocab; t += MAXIDF_THREADS) {
+      const uint32_t d = df8[t];
+      out[t] = logf(n / (float)(d > 1u ? d : 1u));
+    }
+  }
+
+  // ---- pass 2: per-chunk minimum df -------------------------------------
+  const int64_t nvec_seq = L >> 2;
+  const int group = chunk >> 2;  // lanes per chunk (1..64)
+  const int64_t nchunks_seq = L >> chunk_log2;
+  const int4* seq4 = reinterpret_cast<const int4*>(seq);
+  for (int64_t v0 = 0; v0 < nvec_seq; v0 += MAXIDF_THREADS) {
+    const int64_t v = v0 + tid;  // uniform trip count: every lane joins the shuffles
+    uint32_t mn = 255u;
+    if (v < nvec_seq) {
+      const int4 t4 = seq4[v];
+      mn = min(min(df_of(t4.x, vocab, df8), df_of(t4.y, vocab, df8)),
+               min(df_of(t4.z, vocab, df8), df_of(t4.w, vocab, df8)));
+    }
+    for (int off = 1; off < group; off <<= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off, 64));
+    if ((lane & (group - 1)) == 0 && v < nvec_seq) {
+      const int64_t c = v / group;
+      cmin[c] = (uint8_t)mn;
+      if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
+    }
+  }
+  __syncthreads();
+
+  // ---- select: top-k chunks per block, ascending order ------------------
+  if (topk == 0) return;
+  const int C = Lb >> chunk_log2;          // chunks per block
+  const int per_lane = (C + 63) >> 6;      // contiguous chunks owned by a lane
+  for (int j = wave; j < num_blocks; j += MAXIDF_WAVES) {
+    const uint8_t* cv = cmin + (int64_t)j * C;
+    const int c0 = lane * per_lane;
+    const int c1 = min(C, c0 + per_lane);
+    // smallest tau with #(mindf <= tau) >= topk; mindf lies in [1, num_blocks]
+    int lo = 0, hi = num_blocks;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      int cnt = 0;
+      for (int c = c0; c < c1; ++c) cnt += cv[c] <= mid;
+      cnt = wave_sum_int(cnt);
+      if (cnt >= topk) hi = mid; else lo = mid;
+    }
+    const int tau = hi;
+    int n_lt = 0, n_eq = 0;
+    for (int c = c0; c < c1; ++c) {
+      n_lt += cv[c] < tau;
+      n_eq += cv[c] == tau;
+    }
+    const int need = topk - wave_sum_int(n_lt);  // chunks equal to tau that are kept
+    const int eq_base = wave_excl_scan(n_eq);     // equal-to-tau chunks in lower lanes
+    int n_sel = 0;
+    int r = eq_base;
+    for (int c = c0; c < c1; ++c) {
+      const int x = cv[c];
+      if (x < tau) {
+        ++n_sel;
+      } else if (x == tau) {
+        n_sel += r < need;
+        ++r;
+      }
+    }
+    int out = wave_excl_scan(n_sel);
+    int32_t* dst = sel + (b * num_blocks + j) * topk;
+    r = eq_base;
+    for (int c = c0; c < c1; ++c) {
+      const int x = cv[c];
+      bool keep = x < tau;
+      if (x == tau) {
+        keep = r < need;
+        ++r;
+      }
+      if (keep) dst[out++] = c;
+    }
+  }
+}
+
+int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
+                  int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
+                  hipStream_t stream) {
+  if (batch == 0) return PULSAR_OK;
+  int chunk_log2 = 0;
+  while ((1 << chunk_log2) < chunk) ++chunk_log2;
+  if (hipFuncSetAttribute((const void*)maxidf_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)lds_bytes) != hipSuccess)
+    return PULSAR_EHIP;
+  hipLaunchKernelGGL(maxidf_kernel, dim3(batch), dim3(MAXIDF_THREADS), lds_bytes, stream, ids, L,
+                     num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, sel, chunk_mindf,
+                     idf);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}

@@ -1,0 +1,99 @@
+// Bandwidth-bound helper kernels: the materialised Eq. 3 position map, the
+// KV(B_i) retention copy, and the Phase-2 online-softmax merge.
+#include "common.hpp"
+
+// ---------------------------------------------------------------------------
+// Row -> global position map (Eq. 3, sparse position ids).
+__global__ __launch_bounds__(256) void positions_kernel(RowMap mp, const int32_t* __restrict__ sel,
+                                                        int64_t sel_bstride, int n_rows,
+                                                        int32_t* __restrict__ pos) {
+  const int b = blockIdx.y;
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= n_rows) return;
+  pos[(int64_t)b * n_rows + r] = row_position(mp, sel ? sel + b * sel_bstride : nullptr, r);
+}
+
+int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
+                     int n_rows, int32_t* pos, hipStream_t stream) {
+  if (batch == 0 || n_rows == 0) return PULSAR_OK;
+  dim3 grid((n_rows + 255) / 256, batch);
+  hipLaunchKernelGGL(positions_kernel, grid, dim3(256), 0, stream, mp, sel, sel_bstride, n_rows,
+                     pos);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+// ---------------------------------------------------------------------------
+// Strided row copy (KV(B_i) retention, Appendix "KV Cache Discard").  Rows are
+// multiples of 16 bytes and 16-byte aligned (checked by the caller).
+__global__ __launch_bounds__(256) void copy_rows_kernel(const u32x4* __restrict__ src,
+                                                        int64_t src_pitch16,
+                                                        u32x4* __restrict__ dst,
+                                                        int64_t dst_pitch16, int64_t row16) {
+  const int64_t row = blockIdx.y;
+  const u32x4* s = src + row * src_pitch16;
+  u32x4* d = dst + row * dst_pitch16;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < row16;
+       i += (int64_t)gridDim.x * 256)
+    d[i] = s[i];
+}
+
+int launch_copy_rows(const void* src, int64_t src_pitch, void* dst, int64_t dst_pitch,
+                     int64_t bytes_per_row, int rows, hipStream_t stream) {
+  if (rows == 0 || bytes_per_row == 0) return PULSAR_OK;
+  const int64_t row16 = bytes_per_row / 16;
+  int64_t blocks = (row16 + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  hipLaunchKernelGGL(copy_rows_kernel, dim3((unsigned)blocks, rows), dim3(256), 0, stream,
+                     (const u32x4*)src, src_pitch / 16, (u32x4*)dst, dst_pitch / 16, row16);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+// ---------------------------------------------------------------------------
+// Online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
+// Thread = four consecutive head_dim entries of one (z, query, head).
+// l = m + ln sum_h exp(l_h - m) with m = max_h l_h, then
+// o = sum_h exp(l_h - l) o_h; -inf partials weigh zero.
+__global__ __launch_bounds__(256) void lse_merge_kernel(
+    const float* __restrict__ o_parts, const float* __restrict__ lse_parts, int H, int Tq, int Hq,
+    int d4, int64_t part_ostride, int64_t part_lstride, float* __restrict__ o,
+    float* __restrict__ lse, int64_t total) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const int dv = (int)(i % d4);
+  int64_t rest = i / d4;
+  const int h = (int)(rest % Hq);
+  rest /= Hq;
+  const int q = (int)(rest % Tq);
+  const int64_t z = rest / Tq;
+
+  const float* lp = lse_parts + z * (int64_t)H * part_lstride + (int64_t)h * Tq + q;
+  float mx = -INFINITY;
+  for (int p = 0; p < H; ++p) mx = fmaxf(mx, lp[p * part_lstride]);
+  const int64_t orow = (((int64_t)q * Hq + h) * d4 + dv);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float ell = -INFINITY;
+  if (mx != -INFINITY) {
+    float sum = 0.f;
+    for (int p = 0; p < H; ++p) sum += __expf(lp[p * part_lstride] - mx);
+    ell = mx + __logf(sum);
+    const f32x4* op = reinterpret_cast<const f32x4*>(o_parts) + z * (int64_t)H * (part_ostride / 4);
+    for (int p = 0; p < H; ++p) {
+      const float w = __expf(lp[p * part_lstride] - ell);
+      const f32x4 v = op[p * (part_ostride / 4) + orow];
+      acc += w * v;
+    }
+  }
+  reinterpret_cast<f32x4*>(o)[z * (int64_t)Tq * Hq * d4 + orow] = acc;
+  if (lse && dv == 0) lse[z * (int64_t)Hq * Tq + (int64_t)h * Tq + q] = ell;
+}
+
+int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz, int Tq, int Hq,
+                     int d, int64_t part_ostride, int64_t part_lstride, float* o, float* lse,
+                     hipStream_t stream) {
+  const int64_t total = (int64_t)nz * Tq * Hq * (d / 4);
+  if (total == 0) return PULSAR_OK;
+  const int64_t blocks = (total + 255) / 256;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, o_parts,
+                     lse_parts, H, Tq, Hq, d / 4, part_ostride, part_lstride, o, lse, total);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}

@@ -1,0 +1,139 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before any GPU call (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import assembly
+from paper_2607_20457_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pulsar.h")
+
+EINVAL, EUNSUP, EWS = -1, -2, -4
+FAKE = 1 << 20  # a non-NULL, 16-byte aligned address that is never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pulsar_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("pulsar_maxidf_summaries", "pulsar_phase1_attn", "pulsar_phase2_partial",
+              "pulsar_lse_merge"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.lib()
+    names = declared_functions()
+    assert set(names) == set(_lib.SIGNATURES), "binding and header disagree"
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    lib = _lib.lib()
+    assert lib.pulsar_version() >= 1
+    for code in (0, -1, -2, -3, -4, 7):
+        assert isinstance(_lib.status_string(code), str)
+
+
+@pytest.mark.parametrize("L,N,i,s,m,k,mode", [
+    (4096, 4, 3, 64, 16, 4, 0), (32768, 8, 7, 64, 32, 16, 0), (131072, 16, 15, 64, 32, 32, 0),
+    (131072, 16, 15, 64, 32, 32, 1), (131072, 16, 0, 64, 32, 32, 0), (1024, 4, 2, 0, 8, 0, 0),
+    (1024, 4, 3, 256, 8, 32, 0)])
+def test_phase1_len_matches_oracle(L, N, i, s, m, k, mode):
+    got = _lib.lib().pulsar_phase1_len(L, N, i, s, m, k, mode)
+    assert got == assembly.phase1_len(L, N, i, s, m, k, mode)
+
+
+@pytest.mark.parametrize("args", [
+    (4097, 4, 0, 0, 16, 1, 0),      # L % N
+    (4096, 4, 4, 0, 16, 1, 0),      # block index out of range
+    (4096, 4, 1, 2000, 16, 1, 0),   # sink > Lb
+    (4096, 4, 1, 64, 16, 65, 0),    # k * m > Lb
+    (4096, 4, 1, 64, 0, 1, 0),      # chunk 0
+    (4096, 4, 1, 64, 16, 1, 7),     # mode
+    (4096, 0, 0, 0, 16, 1, 0),      # no blocks
+])
+def test_phase1_len_rejects(args):
+    assert _lib.lib().pulsar_phase1_len(*args) == EINVAL
+
+
+def test_maxidf_validation():
+    f = _lib.lib().pulsar_maxidf_summaries
+    ok = dict(ids=FAKE, batch=1, L=4096, N=4, m=16, k=4, V=32000, sel=FAKE)
+    def call(**kw):
+        a = {**ok, **kw}
+        return f(a["ids"], a["batch"], a["L"], a["N"], a["m"], a["k"], a["V"], a["sel"], None,
+                 None, None)
+    assert call(L=4100) == EINVAL
+    assert call(m=24) == EINVAL          # Lb % m
+    assert call(k=65) == EINVAL          # k > chunks per block
+    assert call(k=-1) == EINVAL
+    assert call(ids=None) == EINVAL
+    assert call(ids=FAKE + 4) == EINVAL  # misaligned
+    assert call(sel=None) == EINVAL
+    assert call(V=0) == EINVAL
+    assert call(batch=-1) == EINVAL
+    assert call(N=256, L=256 * 64) == EUNSUP
+    assert call(m=2) == EUNSUP
+    assert call(m=512, L=4 * 1024, k=1) == EUNSUP
+    assert call(V=400000) == EUNSUP      # df table beyond one CU's LDS
+    assert call(batch=0) == 0            # nothing to do
+
+
+def test_attention_validation():
+    f = _lib.lib().pulsar_phase1_attn
+    base = [FAKE, FAKE, FAKE, 1, 4096, 4, 1, 64, 4, 1, 64, 16, 4, FAKE, 0, 0.125,
+            FAKE, 0, None, None, None, None]
+    def call(**kw):
+        a = list(base)
+        for idx, val in kw.items():
+            a[int(idx[1:])] = val
+        return f(*a)
+    assert call(a4=4097) == EINVAL             # L
+    assert call(a5=6, a6=4) == EINVAL          # Hq % Hkv
+    assert call(a7=96) == EUNSUP               # head_dim
+    assert call(a5=12, a6=4) == EUNSUP         # group 3
+    assert call(a13=None) == EINVAL            # selection needed for block 1
+    assert call(a15=0.0) == EINVAL             # scale
+    assert call(a15=float("inf")) == EINVAL
+    assert call(a17=3) == EINVAL               # out dtype
+    assert call(a19=FAKE) == EINVAL            # K_keep without V_keep
+    assert call(a0=None) == EINVAL
+    assert call(a16=FAKE + 2) == EINVAL        # misaligned O
+    assert call(a3=0) == 0                     # empty batch
+
+
+def test_phase2_and_merge_validation():
+    lib = _lib.lib()
+    p = lib.pulsar_phase2_partial
+    assert p(FAKE, FAKE, FAKE, 16, 64, 8192, 32, 7, 128, 0.1, FAKE, FAKE, None, 0, None) == EINVAL
+    assert p(FAKE, FAKE, FAKE, 16, 64, 8192, 32, 8, 80, 0.1, FAKE, FAKE, None, 0, None) == EUNSUP
+    need = lib.pulsar_phase2_workspace_bytes(16, 64, 8192, 32, 8, 128)
+    assert need > 0
+    assert p(FAKE, FAKE, FAKE, 16, 64, 8192, 32, 8, 128, 0.1, FAKE, FAKE, None, 0, None) == EWS
+    assert p(FAKE, FAKE, FAKE, 16, 64, 8192, 32, 8, 128, 0.1, FAKE, FAKE, FAKE, need - 1,
+             None) == EWS
+    assert p(None, FAKE, FAKE, 16, 64, 8192, 32, 8, 128, 0.1, FAKE, FAKE, FAKE, need,
+             None) == EINVAL
+    assert p(FAKE, FAKE, FAKE, 0, 64, 8192, 32, 8, 128, 0.1, FAKE, FAKE, None, 0, None) == 0
+    m = lib.pulsar_lse_merge
+    assert m(FAKE, FAKE, 0, 64, 32, 128, FAKE, FAKE, None) == EINVAL
+    assert m(FAKE, FAKE, 2, 64, 32, 6, FAKE, FAKE, None) == EINVAL
+    assert m(None, FAKE, 2, 64, 32, 128, FAKE, FAKE, None) == EINVAL
+    assert m(FAKE, FAKE, 2, 0, 32, 128, FAKE, FAKE, None) == 0
+
+
+def test_binding_refuses_missing_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError):
+        _lib.lib()

@@ -1,0 +1,143 @@
+"""GPU parity of Phase-1 prefixed-block causal attention (and the Star anchor
+baseline) against the fp64 oracle: O max-abs <= 1e-2 with relative L2 <=
+1e-2, LSE max-abs <= 1e-3; retained KV bit-exact."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_20457_amd as P
+from oracle import assembly, attention, maxidf
+from paper_2607_20457_amd import workload
+from tests._helpers import check_attention, f64, gpu_available, to_dev_bf16, to_dev_i32
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+
+def _inputs(cfg, batch=1, q_scale=1.0):
+    ids = workload.make_ids(cfg, batch=batch)
+    q, k, v = workload.make_qkv(cfg, batch=batch, q_scale=q_scale)
+    sel, _, _, _ = maxidf.maxidf_summaries(ids, cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab)
+    return sel, q, k, v
+
+
+def _run(cfg, i, mode, sel, q, k, v, o_dtype=P.OUT_F32, keep=False):
+    print(f"phase1 parity: {cfg.name} block={i} mode={mode} q={q.shape} o_dtype={o_dtype}",
+          flush=True)
+    res = P.phase1_attn(to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), cfg.num_blocks, i,
+                        cfg.sink, cfg.chunk, cfg.topk, to_dev_i32(sel), mode, o_dtype=o_dtype,
+                        keep_kv=keep)
+    torch.cuda.synchronize()
+    return res
+
+
+def _full_check(cfg, i, mode, sel, q, k, v, b=0):
+    o, lse = _run(cfg, i, mode, sel, q, k, v)
+    pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk,
+                                    sel[b], mode)
+    o_ref, lse_ref = attention.phase1_attention(f64(q[b]), f64(k[b]), f64(v[b]), pos,
+                                                1 / math.sqrt(cfg.d))
+    check_attention(o[b].cpu().numpy(), lse[b].cpu().numpy(), o_ref, lse_ref,
+                    f"{cfg.name} block {i} mode {mode}")
+
+
+def _sampled_check(cfg, i, mode, sel, q, k, v, rows, b=0):
+    o, lse = _run(cfg, i, mode, sel, q, k, v)
+    pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk,
+                                    sel[b], mode)
+    rows = np.array(sorted(set(int(r) for r in rows if 0 <= r < len(pos))))
+    o_ref, lse_ref = attention.phase1_attention(f64(q[b]), f64(k[b]), f64(v[b]), pos,
+                                                1 / math.sqrt(cfg.d), rows=rows)
+    check_attention(o[b, rows].cpu().numpy(), lse[b][:, rows].cpu().numpy(), o_ref, lse_ref,
+                    f"{cfg.name} block {i} mode {mode} sampled")
+
+
+def test_tiny_all_blocks_full():
+    cfg = workload.CONFIGS["tiny"]
+    sel, q, k, v = _inputs(cfg)
+    for i in range(cfg.num_blocks):
+        _full_check(cfg, i, P.PREFIX_SUMMARY, sel, q, k, v)
+    _full_check(cfg, 3, P.PREFIX_ANCHOR, sel, q, k, v)
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(8, 2), (4, 4), (16, 2)])
+def test_ragged_gqa_shapes_full(Hq, Hkv):
+    # n_i = 1000 + 40 + i*60: not a multiple of the 32-row or 64-key tiles
+    cfg = workload.Config("ragged", L=4000, vocab=5000, num_blocks=4, sink=40, chunk=20,
+                          topk=3, Hq=Hq, Hkv=Hkv, d=128, batch=2, seed=31)
+    ids = workload.make_ids(cfg)
+    q, k, v = workload.make_qkv(cfg)
+    rng = np.random.default_rng(3)
+    sel = np.sort(np.stack([[rng.choice(50, 3, replace=False) for _ in range(4)]
+                            for _ in range(2)]), axis=2)
+    for i in (1, 3):
+        _full_check(cfg, i, P.PREFIX_SUMMARY, sel, q, k, v, b=1)
+    assert ids.shape == (2, 4000)
+
+
+def test_llama8b_32k_every_block_sampled():
+    cfg = workload.CONFIGS["llama8b_32k"]
+    sel, q, k, v = _inputs(cfg)
+    for i in range(cfg.num_blocks):
+        n = assembly.phase1_len(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk)
+        rows = [0, 1, 63, 64, cfg.sink, cfg.sink + 1, n // 2, n - cfg.Lb - 1, n - cfg.Lb,
+                n - 2, n - 1]
+        _sampled_check(cfg, i, P.PREFIX_SUMMARY, sel, q, k, v, rows)
+
+
+def test_llama8b_128k_block15_sampled():
+    # the full-size headline launch: block 15 of 16, n = 23616
+    cfg = workload.CONFIGS["llama8b_128k"]
+    sel, q, k, v = _inputs(cfg)
+    n = assembly.phase1_len(cfg.L, 16, 15, cfg.sink, cfg.chunk, cfg.topk)
+    assert n == 23616
+    rng = np.random.default_rng(15)
+    rows = [0, 63, 64, 65, 1087, 1088, 15423, 15424, n - 1] + list(rng.integers(0, n, 8))
+    _sampled_check(cfg, 15, P.PREFIX_SUMMARY, sel, q, k, v, rows)
+    _sampled_check(cfg, 15, P.PREFIX_ANCHOR, sel, q, k, v, [0, 8191, 8192, 16383])
+
+
+def test_peaked_attention_control():
+    # Q scaled by 8: softmax mass concentrates, |O| ~ 1, so a zero or shifted
+    # output cannot pass the absolute tolerance
+    cfg = workload.Config("peaked", L=8192, vocab=4000, num_blocks=4, sink=64, chunk=32,
+                          topk=8, Hq=8, Hkv=2, d=128, seed=41)
+    sel, q, k, v = _inputs(cfg, q_scale=8.0)
+    o, _ = _run(cfg, 2, P.PREFIX_SUMMARY, sel, q, k, v)
+    assert float(o.abs().mean()) > 0.2
+    _full_check(cfg, 2, P.PREFIX_SUMMARY, sel, q, k, v)
+
+
+def test_bf16_output_and_kept_kv():
+    cfg = workload.CONFIGS["tiny"]
+    sel, q, k, v = _inputs(cfg)
+    o32, lse32 = _run(cfg, 2, P.PREFIX_SUMMARY, sel, q, k, v)
+    o16, lse16, kk, vk = _run(cfg, 2, P.PREFIX_SUMMARY, sel, q, k, v, o_dtype=P.OUT_BF16,
+                              keep=True)
+    # bf16 output is the fp32 output rounded once (half an ulp of bf16)
+    ref = o32.to(torch.bfloat16)
+    assert torch.equal(o16, ref)
+    assert torch.equal(lse16, lse32)
+    Lb = cfg.Lb
+    assert torch.equal(kk.cpu().view(torch.int16),
+                       torch.from_numpy(k[:, 2 * Lb:3 * Lb].view(np.int16)))
+    assert torch.equal(vk.cpu().view(torch.int16),
+                       torch.from_numpy(v[:, 2 * Lb:3 * Lb].view(np.int16)))
+
+
+def test_degenerate_sink_and_k_zero():
+    cfg = workload.Config("deg", L=2048, vocab=1000, num_blocks=4, sink=0, chunk=16, topk=0,
+                          Hq=4, Hkv=1, d=64, seed=51)
+    q, k, v = workload.make_qkv(cfg)
+    sel = np.zeros((1, 4, 0), dtype=np.int32)
+    _full_check(cfg, 3, P.PREFIX_SUMMARY, sel, q, k, v)
+
+
+def test_deterministic():
+    cfg = workload.CONFIGS["tiny"]
+    sel, q, k, v = _inputs(cfg)
+    a = _run(cfg, 3, P.PREFIX_SUMMARY, sel, q, k, v)
+    b = _run(cfg, 3, P.PREFIX_SUMMARY, sel, q, k, v)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])

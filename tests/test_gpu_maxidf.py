@@ -1,0 +1,123 @@
+"""GPU parity of Max-IDF selection and the Eq. 3 position map against the
+fp64 oracle.  Selections, chunk minima and positions must match bit for bit."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_20457_amd as P
+from oracle import assembly, maxidf
+from paper_2607_20457_amd import workload
+from tests._helpers import gpu_available, to_dev_i32
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+
+def _check(ids, N, m, k, V, idf_too=True):
+    print(f"maxidf parity: batch={ids.shape[0]} L={ids.shape[1]} N={N} m={m} k={k} V={V}",
+          flush=True)
+    sel_ref, mindf_ref, idf_ref, _ = maxidf.maxidf_summaries(ids, N, m, k, V)
+    d_ids = to_dev_i32(ids)
+    if idf_too:
+        sel, mindf, idf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True, return_idf=True)
+    else:
+        sel, mindf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(mindf.cpu().numpy(), mindf_ref)
+    assert np.array_equal(sel.cpu().numpy(), sel_ref)
+    if idf_too:
+        np.testing.assert_allclose(idf.cpu().numpy(), idf_ref, rtol=2e-6, atol=2e-6)
+    return sel
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b_32k", "llama8b_128k"])
+def test_config_workloads(name):
+    cfg = workload.CONFIGS[name]
+    ids = workload.make_ids(cfg, batch=1)
+    _check(ids, cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab)
+
+
+def test_needles_config_selects_planted_needles_when_discriminative():
+    # V=512 background: no natural df=1 ids, so every planted needle chunk wins
+    cfg = workload.Config("needles512", L=32768, vocab=512, num_blocks=8, sink=64, chunk=32,
+                          topk=16, Hq=1, Hkv=1, d=64)
+    base = workload.zipf_ids(77, cfg.L, 512)
+    ids, _, pos = workload.plant_needles(78, base, 16, 1024)
+    sel = _check(ids[None], 8, 32, 16, 1024)[0].cpu().numpy()
+    for p in pos:
+        assert (p % cfg.Lb) // 32 in sel[p // cfg.Lb]
+
+
+@pytest.mark.parametrize("vocab,N,L", [(512, 8, 32768), (2048, 8, 32768), (512, 16, 131072),
+                                       (2048, 16, 131072)])
+def test_discriminative_vocab(vocab, N, L):
+    ids = np.stack([workload.zipf_ids(1000 + vocab + b, L, vocab) for b in range(2)])
+    _check(ids, N, 32, 16, vocab)
+
+
+@pytest.mark.parametrize("m", [4, 8, 16, 64, 128, 256])
+def test_chunk_sizes(m):
+    L, N = 8192, 4
+    ids = workload.zipf_ids(500 + m, L, 700)[None]
+    C = L // N // m
+    for k in sorted({0, 1, C // 3, C}):
+        _check(ids, N, m, k, 700, idf_too=False)
+
+
+def test_batch8_at_128k():
+    cfg = workload.CONFIGS["sweep_128k_b4"]
+    ids = workload.make_ids(cfg, batch=8)
+    _check(ids, cfg.num_blocks, cfg.chunk, 32, cfg.vocab, idf_too=False)
+
+
+def test_single_block_and_adversarial_contention():
+    ids = workload.zipf_ids(9, 4096, 3000)[None]
+    sel = _check(ids, 1, 16, 7, 3000)
+    assert sel.cpu().numpy()[0, 0].tolist() == list(range(7))
+    same = np.full((1, 8192), 17, dtype=np.int32)            # every lane hits one LDS word
+    _check(same, 8, 32, 5, 64)
+    two = (np.arange(16384, dtype=np.int32) % 2)[None] * 1000  # two-token alphabet
+    _check(two, 16, 16, 3, 1001)
+    ragged_vocab = workload.zipf_ids(10, 6144, 33)[None]      # vocab not a multiple of 4 or 32
+    _check(ragged_vocab, 3, 32, 2, 33)
+
+
+def test_max_blocks_and_large_vocab():
+    ids = workload.zipf_ids(21, 255 * 64, 140000)[None]     # N = 255, the df byte's limit
+    _check(ids, 255, 16, 1, 140000, idf_too=False)
+
+
+def test_deterministic():
+    ids = to_dev_i32(workload.make_ids(workload.CONFIGS["llama8b_32k"], batch=2))
+    a = P.maxidf_summaries(ids, 8, 32, 16, 128256, return_mindf=True)
+    b = P.maxidf_summaries(ids, 8, 32, 16, 128256, return_mindf=True)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("mode", [assembly.PREFIX_SUMMARY, assembly.PREFIX_ANCHOR])
+def test_positions_match_eq3(mode):
+    cfg = workload.CONFIGS["llama8b_32k"]
+    ids = workload.make_ids(cfg, batch=2)
+    sel_ref, _, _, _ = maxidf.maxidf_summaries(ids, cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab)
+    sel = to_dev_i32(sel_ref)
+    for i in range(cfg.num_blocks):
+        pos = P.phase1_positions(sel, 2, cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk,
+                                 cfg.topk, mode).cpu().numpy()
+        for b in range(2):
+            ref = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk,
+                                            cfg.topk, sel_ref[b], mode)
+            assert np.array_equal(pos[b], ref)
+
+
+def test_positions_ragged_shapes():
+    L, N, s, m, k = 3 * 1000, 3, 40, 20, 7
+    rng = np.random.default_rng(4)
+    sel_ref = np.sort(np.stack([rng.choice(1000 // m, k, replace=False) for _ in range(N)]),
+                      axis=1)[None]
+    sel = to_dev_i32(sel_ref)
+    for i in range(N):
+        pos = P.phase1_positions(sel, 1, L, N, i, s, m, k).cpu().numpy()[0]
+        assert np.array_equal(pos, assembly.phase1_positions(L, N, i, s, m, k, sel_ref[0]))
+    assert math.isfinite(float(pos.sum()))
