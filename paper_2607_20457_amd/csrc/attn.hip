@@ -20,6 +20,9 @@
 //                 only raised when it grows by more than 2^8 (the final
 //                 normalisation divides by a sum taken with the same max, so
 //                 the result is unchanged and the O rescale is rare).
+//                 P enters the PV product rounded to bf16; O is divided by the
+//                 sum of those rounded weights (so they form an exact convex
+//                 combination), while the LSE uses the fp32 sum.
 //   O^T += V^T P^T  A = V^T from LDS (V is transposed on its way into LDS),
 //                 B = P, which is already in the B-operand layout because K
 //                 rows are stored in LDS with bits 2 and 3 of the key index
@@ -33,6 +36,8 @@ namespace {
 constexpr int BN = 64;          // keys per tile
 constexpr int THREADS = 256;    // 4 wavefronts
 constexpr float MAX_SLACK = 8.0f;  // log2-domain slack before the running max is raised
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 
 template <int D>
 struct Tile {
@@ -138,11 +143,12 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
   for (int e = 0; e < DT; ++e)
 #pragma unroll
     for (int t = 0; t < QT; ++t) acc[e][t] = f32x16{};
-  float m_run[QT], l_run[QT];
+  float m_run[QT], l_run[QT], lr_run[QT];  // max, fp32 weight sum, bf16-rounded weight sum
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     m_run[t] = -INFINITY;
     l_run[t] = 0.f;
+    lr_run[t] = 0.f;
   }
 
   // ---- cooperative tile loads -----------------------------------------------
@@ -265,10 +271,11 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
         const bool raise = m_new > m_run[t] + MAX_SLACK;
         const float m_use = raise ? m_new : m_run[t];
         if (__any(raise)) {
-          const float alpha = exp2f(m_run[t] - m_use);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_use);
 #pragma unroll
           for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
           l_run[t] *= alpha;
+          lr_run[t] *= alpha;
         }
         m_run[t] = m_use;
         float psum = 0.f;
@@ -279,10 +286,15 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
             f32x8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
-              p[v] = exp2f(__builtin_fmaf(S[u][t][8 * c + v], a.scale_log2, -m_use));
+              p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[u][t][8 * c + v], a.scale_log2, -m_use));
               psum += p[v];
             }
             pf[u][c][t] = __builtin_convertvector(p, bf16x8);
+            const bf16x8 w = pf[u][c][t];
+#pragma unroll
+            for (int v = 0; v < 8; v += 2)
+              lr_run[t] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[v], w[v + 1]}, kOnes2,
+                                                          lr_run[t], false);
           }
         l_run[t] += psum;
       }
@@ -308,7 +320,8 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const float l_tot = l_run[t] + __shfl_xor(l_run[t], 32, 64);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float lr_tot = lr_run[t] + __shfl_xor(lr_run[t], 32, 64);
+    const float inv = lr_tot > 0.f ? 1.f / lr_tot : 0.f;
     const int qrow = row0 + t * 32 + l32;
     if (qrow < a.n_q) {
       const int64_t obase = ((int64_t)z * a.o_zstride) + ((int64_t)qrow * a.Hq + head) * D;
