@@ -185,7 +185,7 @@ static int phase2_splits(int n_shards, int Tq, int64_t S, int Hq, int Hkv) {
   if (S <= 0) return 1;
   const int group = Hq / Hkv;
   const int heads_per_wg = group >= 4 ? 4 : group;
-  const int rows_per_wg = 32 * (4 / heads_per_wg);
+  const int rows_per_wg = attn_rows_per_wg(group);
   const int64_t row_tiles = (Tq + rows_per_wg - 1) / rows_per_wg;
   const int64_t base = row_tiles * (group / heads_per_wg) * Hkv * n_shards;
   const int64_t target = 2048;  // about 8 workgroups per compute unit

@@ -13,15 +13,19 @@
 //   Workgroup ids run heaviest causal row tile first, and the KV head is the
 //   fastest-varying index, so with 8 KV heads each XCD's L2 serves one head.
 //
-// Per wavefront, per 64-key tile (32x32x16 bf16 MFMA, fp32 accumulate)
+// Per wavefront, per 64-key tile, in two 32-key halves (32x32x16 bf16 MFMA,
+// fp32 accumulate)
 //   S^T = K Q^T   A = K rows from LDS, B = Q fragments held in registers;
-//                 the lane of query q holds 16 scores of q per 32-key block.
-//   online softmax in the log2 domain on those registers; the running max is
-//                 only raised when it grows by more than 2^8 (the final
-//                 normalisation divides by a sum taken with the same max, so
-//                 the result is unchanged and the O rescale is rare).
-//                 P enters the PV product rounded to bf16; O is divided by the
-//                 sum of those rounded weights (so they form an exact convex
+//                 the lane of query q holds 16 scores of q per half.
+//   softmax       log2 domain.  Scores are taken relative to a fixed per-row
+//                 reference (the row's maximum over the first 32 keys), so the
+//                 O accumulator is only ever touched by the matrix cores; the
+//                 final division by the weight sum makes the result exact.
+//                 Should a weight exceed 2^64 (a later score far above the
+//                 reference), the workgroup repeats the pass with the classic
+//                 online softmax, which raises the running maximum and
+//                 rescales O.  P enters the PV product rounded to bf16; O is
+//                 divided by the sum of those rounded weights (an exact convex
 //                 combination), while the LSE uses the fp32 sum.
 //   O^T += V^T P^T  A = V^T from LDS (V is transposed on its way into LDS),
 //                 B = P, which is already in the B-operand layout because K
@@ -29,13 +33,15 @@
 //                 swapped.
 //   K/V tiles are double-buffered: the next tile's global loads are issued
 //   before the current tile's math and written to LDS after it.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace {
 
 constexpr int BN = 64;          // keys per tile
 constexpr int THREADS = 256;    // 4 wavefronts
-constexpr float MAX_SLACK = 8.0f;  // log2-domain slack before the running max is raised
+constexpr float MAX_SLACK = 8.0f;  // exact pass: log2 slack before the running max is raised
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 __device__ constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 
@@ -48,10 +54,7 @@ struct Tile {
   static constexpr int STAGE = K_BYTES + V_BYTES;
   static constexpr int LDS = 2 * STAGE + 2 * BN * 4;  // two stages + two position rows
   static constexpr int CPR = D / 8;               // 16-byte chunks per row
-  static constexpr int K_ROWS_PER_PASS = THREADS / CPR;
-  static constexpr int K_PASSES = BN / K_ROWS_PER_PASS;
-  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit
-  static constexpr int V_PASSES = (V_UNITS + THREADS - 1) / THREADS;
+  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= THREADS)
 };
 
 struct KernelArgs {
@@ -76,11 +79,13 @@ __device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
 }
 
 template <int D, int QT, bool CAUSAL>
-__global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(3 - QT, 3 - QT)))
+void attn_fwd_kernel(KernelArgs ka) {
   using T = Tile<D>;
   constexpr int QR = 32 * QT;        // rows per wavefront
   constexpr int DS = D / 16;         // k-steps of the S product
   constexpr int DT = D / 32;         // 32-row tiles of O^T
+  constexpr int KR = BN * T::CPR / THREADS;  // consecutive K rows loaded per thread
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const AttnLaunch& a = ka.a;
 
@@ -118,6 +123,7 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
   const uint16_t* Qz = a.Q + zkv * a.q_zstride + (int64_t)head * D;
   const uint16_t* Kz = a.K + zkv * a.kv_zstride + (int64_t)kvh * D;
   const uint16_t* Vz = a.V + zkv * a.kv_zstride + (int64_t)kvh * D;
+  const float c2 = a.scale_log2;
 
   uint8_t* stage0 = smem;
   int32_t* lpos = reinterpret_cast<int32_t*>(smem + 2 * T::STAGE);  // [2][BN]
@@ -127,193 +133,212 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const int r = row0 + t * 32 + l32;
-    if (r < a.n_q) {
-      const int p = row_position(a.map, sel, r);
-      const bf16x8* src = reinterpret_cast<const bf16x8*>(Qz + (int64_t)p * q_row) + g;
+    const int p = r < a.n_q ? row_position(a.map, sel, r) : 0;
+    const bf16x8* src = reinterpret_cast<const bf16x8*>(Qz + (int64_t)p * q_row) + g;
 #pragma unroll
-      for (int s = 0; s < DS; ++s) qf[t][s] = src[2 * s];
-    } else {
-#pragma unroll
-      for (int s = 0; s < DS; ++s) qf[t][s] = bf16x8{};
-    }
+    for (int s = 0; s < DS; ++s) qf[t][s] = r < a.n_q ? src[2 * s] : bf16x8{};
   }
+  // Drain the Q loads here, so that no wait inside the key loop is tied to them.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
   f32x16 acc[DT][QT];
-#pragma unroll
-  for (int e = 0; e < DT; ++e)
-#pragma unroll
-    for (int t = 0; t < QT; ++t) acc[e][t] = f32x16{};
-  float m_run[QT], l_run[QT], lr_run[QT];  // max, fp32 weight sum, bf16-rounded weight sum
-#pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    m_run[t] = -INFINITY;
-    l_run[t] = 0.f;
-    lr_run[t] = 0.f;
-  }
+  float m_ref[QT], l_run[QT], lr_run[QT];  // reference max, fp32 weight sum, bf16 weight sum
 
   // ---- cooperative tile loads -----------------------------------------------
+  // K: thread t loads rows KR*(t/CPR) .. +KR-1 at 16-byte chunk t%CPR.
+  // V: thread t (t < 16*CPR) loads rows 4*(t%16) .. +3 at chunk t/16 and
+  //    writes them transposed (head_dim-major) into LDS.
   auto tile_positions = [&](int j, int32_t* dst) {
     if (tid < BN) {
       const int k = kv_begin + j * BN + tid;
       dst[tid] = k < kv_end ? row_position(a.map, sel, k) : -1;
     }
   };
-  u32x4 kreg[T::K_PASSES];
-  u32x4 vreg[T::V_PASSES][4];
+  u32x4 kreg[KR];
+  u32x4 vreg[4];
+  int vpos[4];  // kept to zero the V rows of padded keys when they are stored
+  const bool v_thread = tid < T::V_UNITS;
   auto load_regs = [&](const int32_t* pos) {
+    const int kr0 = KR * (tid / T::CPR);
+    int kp[KR];
+    if constexpr (KR == 4) {
+      const int4 p4 = *reinterpret_cast<const int4*>(pos + kr0);
+      kp[0] = p4.x; kp[1] = p4.y; kp[2] = p4.z; kp[3] = p4.w;
+    } else {
 #pragma unroll
-    for (int it = 0; it < T::K_PASSES; ++it) {
-      const int r = it * T::K_ROWS_PER_PASS + tid / T::CPR;
-      const int p = pos[r];
-      kreg[it] = p >= 0 ? *reinterpret_cast<const u32x4*>(Kz + (int64_t)p * kv_row +
-                                                           (tid % T::CPR) * 8)
-                        : u32x4{0u, 0u, 0u, 0u};
+      for (int i = 0; i < KR; ++i) kp[i] = pos[kr0 + i];
     }
 #pragma unroll
-    for (int it = 0; it < T::V_PASSES; ++it) {
-      const int u = tid + it * THREADS;
-      if (u < T::V_UNITS) {
-        const int kq = u & 15;
-        const int dc = u >> 4;
+    for (int i = 0; i < KR; ++i)
+      kreg[i] = *reinterpret_cast<const u32x4*>(Kz + (int64_t)max(kp[i], 0) * kv_row +
+                                                (tid % T::CPR) * 8);
+    if (v_thread) {
+      const int4 p4 = *reinterpret_cast<const int4*>(pos + 4 * (tid & 15));
+      vpos[0] = p4.x; vpos[1] = p4.y; vpos[2] = p4.z; vpos[3] = p4.w;
+      const int dc = tid >> 4;
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          const int p = pos[4 * kq + rr];
-          vreg[it][rr] = p >= 0 ? *reinterpret_cast<const u32x4*>(Vz + (int64_t)p * kv_row + dc * 8)
-                                : u32x4{0u, 0u, 0u, 0u};
-        }
-      }
+      for (int rr = 0; rr < 4; ++rr)
+        vreg[rr] = *reinterpret_cast<const u32x4*>(Vz + (int64_t)max(vpos[rr], 0) * kv_row + dc * 8);
     }
   };
   auto store_lds = [&](uint8_t* st) {
+    const int kr0 = KR * (tid / T::CPR);
 #pragma unroll
-    for (int it = 0; it < T::K_PASSES; ++it) {
-      const int r = it * T::K_ROWS_PER_PASS + tid / T::CPR;
-      *reinterpret_cast<u32x4*>(st + swap_bits23(r) * T::K_STRIDE + (tid % T::CPR) * 16) = kreg[it];
-    }
-    uint8_t* sv = st + T::K_BYTES;
+    for (int i = 0; i < KR; ++i)
+      *reinterpret_cast<u32x4*>(st + swap_bits23(kr0 + i) * T::K_STRIDE + (tid % T::CPR) * 16) =
+          kreg[i];
+    if (v_thread) {
+      // rows past the end become zero, so that a zero weight never meets a
+      // non-finite value
 #pragma unroll
-    for (int it = 0; it < T::V_PASSES; ++it) {
-      const int u = tid + it * THREADS;
-      if (u < T::V_UNITS) {
-        const int kq = u & 15;
-        const int dc = u >> 4;
-        const u32x4* r4 = vreg[it];
+      for (int rr = 0; rr < 4; ++rr)
+        if (vpos[rr] < 0) vreg[rr] = u32x4{0u, 0u, 0u, 0u};
+      uint8_t* sv = st + T::K_BYTES;
+      const int kq = tid & 15;
+      const int dc = tid >> 4;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
-          const u32x2 lo = {pack_lo(r4[0][w], r4[1][w]), pack_lo(r4[2][w], r4[3][w])};
-          const u32x2 hi = {pack_hi(r4[0][w], r4[1][w]), pack_hi(r4[2][w], r4[3][w])};
-          *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
-          *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
-        }
+      for (int w = 0; w < 4; ++w) {
+        // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
+        const u32x2 lo = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x05040100u),
+                          __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x05040100u)};
+        const u32x2 hi = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x07060302u),
+                          __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x07060302u)};
+        *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
+        *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
       }
     }
   };
 
-  if (ntiles > 0) {
-    tile_positions(0, lpos);
-    __syncthreads();
-    if (ntiles > 1) tile_positions(1, lpos + BN);
-    load_regs(lpos);
-    store_lds(stage0);
-  }
+  // ---- one pass over all key tiles ------------------------------------------
+  // EXACT = false: every row's scores are taken relative to a fixed reference
+  //   (the maximum over the first 32 keys), so the accumulator is never
+  //   rescaled.  A weight above 2^64 flags the pass as unsafe.
+  // EXACT = true: classic online softmax that raises the running maximum when
+  //   it grows by more than 2^8 and rescales the accumulator; it runs only
+  //   for workgroups whose first pass was flagged.
+  auto pass = [&](auto exact_tag) -> bool {
+    constexpr bool EXACT = decltype(exact_tag)::value;
+    bool overflow = false;
+#pragma unroll
+    for (int e = 0; e < DT; ++e)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) acc[e][t] = f32x16{};
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      m_ref[t] = -INFINITY;
+      l_run[t] = 0.f;
+      lr_run[t] = 0.f;
+    }
+    if (ntiles > 0) {
+      tile_positions(0, lpos);
+      __syncthreads();
+      if (ntiles > 1) tile_positions(1, lpos + BN);
+      load_regs(lpos);
+      store_lds(stage0);
+    }
+    for (int j = 0; j < ntiles; ++j) {
+      __syncthreads();
+      const int buf = j & 1;
+      if (j + 1 < ntiles) load_regs(lpos + ((j + 1) & 1) * BN);
+      if (j + 2 < ntiles) tile_positions(j + 2, lpos + buf * BN);
 
-  // ---- main loop over key tiles ---------------------------------------------
-  for (int j = 0; j < ntiles; ++j) {
-    __syncthreads();
-    const int buf = j & 1;
-    if (j + 1 < ntiles) load_regs(lpos + ((j + 1) & 1) * BN);
-    if (j + 2 < ntiles) tile_positions(j + 2, lpos + buf * BN);
-
-    const int kbase = kv_begin + j * BN;
-    const bool wave_active = !CAUSAL || kbase <= row0 + QR - 1;
-    if (wave_active) {
+      const int kbase = kv_begin + j * BN;
       const uint8_t* sK = stage0 + buf * T::STAGE;
       const uint8_t* sV = sK + T::K_BYTES;
-
-      f32x16 S[2][QT];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
+        const int kh = kbase + 32 * u;  // first key of this 32-key half
+        if (CAUSAL && kh > row0 + QR - 1) continue;  // all masked for this wave
+        f32x16 S[QT];
 #pragma unroll
-        for (int t = 0; t < QT; ++t) S[u][t] = f32x16{};
+        for (int t = 0; t < QT; ++t) S[t] = f32x16{};
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
           const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
                                                              (16 * s + 8 * g) * 2);
 #pragma unroll
           for (int t = 0; t < QT; ++t)
-            S[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[u][t], 0, 0, 0);
+            S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[t], 0, 0, 0);
         }
-      }
 
-      const bool edge = CAUSAL ? (kbase + BN - 1 > row0) : (kbase + BN > kv_end);
-      bf16x8 pf[2][2][QT];
-#pragma unroll
-      for (int t = 0; t < QT; ++t) {
+        const bool edge = CAUSAL ? (kh + 31 > row0) : (kh + 32 > kv_end);
         if (edge) {
-          const int qrow = row0 + t * 32 + l32;
 #pragma unroll
-          for (int u = 0; u < 2; ++u)
+          for (int t = 0; t < QT; ++t) {
+            const int qrow = row0 + t * 32 + l32;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-              const int key = kbase + u * 32 + 16 * (v >> 3) + 8 * g + (v & 7);
+              const int key = kh + 16 * (v >> 3) + 8 * g + (v & 7);
               const bool masked = CAUSAL ? (key > qrow || key >= kv_end) : (key >= kv_end);
-              if (masked) S[u][t][v] = -INFINITY;
+              if (masked) S[t][v] = -INFINITY;
             }
+          }
         }
-        float mx = -INFINITY;
+        const bool first = j == 0 && u == 0;
+        bf16x8 pf[2][QT];
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
+        for (int t = 0; t < QT; ++t) {
+          if (EXACT || first) {
+            float mx = S[t][0];
 #pragma unroll
-          for (int v = 0; v < 16; ++v) mx = fmaxf(mx, S[u][t][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = mx * a.scale_log2;
-        const bool raise = m_new > m_run[t] + MAX_SLACK;
-        const float m_use = raise ? m_new : m_run[t];
-        if (__any(raise)) {
-          const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_use);
+            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, S[t][v]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+            if (!EXACT) {
+              m_ref[t] = mx;
+            } else {
+              const bool raise = mx > m_ref[t] + MAX_SLACK;
+              const float m_use = raise ? mx : m_ref[t];
+              if (__any(raise)) {
+                const float alpha = __builtin_amdgcn_exp2f(m_ref[t] - m_use);
 #pragma unroll
-          for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
-          l_run[t] *= alpha;
-          lr_run[t] *= alpha;
-        }
-        m_run[t] = m_use;
-        float psum = 0.f;
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
+                for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
+                l_run[t] *= alpha;
+                lr_run[t] *= alpha;
+              }
+              m_ref[t] = m_use;
+            }
+          }
+          float psum = 0.f;
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
             f32x8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
-              p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[u][t][8 * c + v], a.scale_log2, -m_use));
+              p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[t][8 * c + v], c2, -m_ref[t]));
               psum += p[v];
             }
-            pf[u][c][t] = __builtin_convertvector(p, bf16x8);
-            const bf16x8 w = pf[u][c][t];
+            pf[c][t] = __builtin_convertvector(p, bf16x8);
+            const bf16x8 w = pf[c][t];
 #pragma unroll
             for (int v = 0; v < 8; v += 2)
               lr_run[t] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[v], w[v + 1]}, kOnes2,
                                                           lr_run[t], false);
           }
-        l_run[t] += psum;
-      }
+          l_run[t] += psum;
+          if (!EXACT) overflow |= !(psum <= 0x1p64f);  // also true for inf
+        }
 
 #pragma unroll
-      for (int e = 0; e < DT; ++e)
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
+        for (int e = 0; e < DT; ++e)
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
             const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
                 sV + (e * 32 + l32) * T::V_STRIDE + (u * 32 + 16 * c + 8 * g) * 2);
 #pragma unroll
             for (int t = 0; t < QT; ++t)
-              acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u][c][t], acc[e][t], 0, 0, 0);
+              acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c][t], acc[e][t], 0, 0, 0);
           }
-    }
+      }
 
-    if (j + 1 < ntiles) store_lds(stage0 + (buf ^ 1) * T::STAGE);
+      if (j + 1 < ntiles) store_lds(stage0 + (buf ^ 1) * T::STAGE);
+    }
+    return overflow;
+  };
+
+  const bool ovf = pass(std::false_type{});
+  if (__syncthreads_or(ovf)) {
+    __syncthreads();
+    pass(std::true_type{});
   }
 
   // ---- epilogue: normalise, write O and LSE ---------------------------------
@@ -340,7 +365,7 @@ __global__ __launch_bounds__(THREADS) void attn_fwd_kernel(KernelArgs ka) {
           }
         }
       if (a.lse && g == 0) {
-        const float lse = l_tot > 0.f ? (m_run[t] + __log2f(l_tot)) * 0.69314718055994531f
+        const float lse = l_tot > 0.f ? (m_ref[t] + __log2f(l_tot)) * 0.69314718055994531f
                                       : -INFINITY;
         a.lse[(int64_t)z * a.lse_zstride + (int64_t)head * a.n_q + qrow] = lse;
       }
@@ -363,18 +388,31 @@ int launch_impl(const KernelArgs& ka, hipStream_t stream) {
 
 }  // namespace
 
+// Queries per wavefront = 32 * QT.  QT = 2 halves the LDS traffic per matrix
+// instruction (each K/V fragment read from LDS feeds two products) but needs
+// the whole register file of a SIMD; QT = 1 runs two wavefronts per SIMD.
+#ifndef PULSAR_ATTN_QT
+#define PULSAR_ATTN_QT 1
+#endif
+constexpr int kQT = PULSAR_ATTN_QT;
+
+int attn_rows_per_wg(int group) {
+  const int heads_per_wg = group >= 4 ? 4 : group;
+  return 32 * kQT * (4 / heads_per_wg);
+}
+
 int launch_attention(const AttnLaunch& a, hipStream_t stream) {
   KernelArgs ka;
   ka.a = a;
   ka.group = a.Hq / a.Hkv;
   ka.heads_per_wg = ka.group >= 4 ? 4 : ka.group;
   ka.hsub = ka.group / ka.heads_per_wg;
-  constexpr int QT = 1;
-  ka.rows_per_wg = 32 * QT * (4 / ka.heads_per_wg);
+  ka.rows_per_wg = attn_rows_per_wg(ka.group);
   ka.n_row_tiles = (a.n_q + ka.rows_per_wg - 1) / ka.rows_per_wg;
   ka.nz = a.nz_kv * a.nsplit;
   if (a.d == 128) {
-    return a.causal ? launch_impl<128, QT, true>(ka, stream) : launch_impl<128, QT, false>(ka, stream);
+    return a.causal ? launch_impl<128, kQT, true>(ka, stream)
+                    : launch_impl<128, kQT, false>(ka, stream);
   }
-  return a.causal ? launch_impl<64, QT, true>(ka, stream) : launch_impl<64, QT, false>(ka, stream);
+  return a.causal ? launch_impl<64, kQT, true>(ka, stream) : launch_impl<64, kQT, false>(ka, stream);
 }

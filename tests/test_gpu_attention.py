@@ -141,3 +141,20 @@ def test_deterministic():
     a = _run(cfg, 3, P.PREFIX_SUMMARY, sel, q, k, v)
     b = _run(cfg, 3, P.PREFIX_SUMMARY, sel, q, k, v)
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_far_larger_later_score_takes_exact_pass():
+    # A key placed after the first 32 keys whose score exceeds the first keys'
+    # maximum by far more than 2^64 in weight: the reference-max pass flags
+    # it and the exact online-softmax pass must give the oracle's answer.
+    cfg = workload.Config("spike", L=2048, vocab=1000, num_blocks=2, sink=16, chunk=16,
+                          topk=2, Hq=4, Hkv=1, d=64, seed=61)
+    q, k, v = workload.make_qkv(cfg)
+    qf = workload.bf16_bits_to_f32(q) + 1.0          # queries share a mean direction
+    q = workload.f32_to_bf16_bits(qf)
+    kf = workload.bf16_bits_to_f32(k)
+    kf[0, 500] = 10.0                                # q.k / sqrt(d) ~ 80 for that key
+    k = workload.f32_to_bf16_bits(kf)
+    sel = np.array([[[0, 5], [1, 2]]], dtype=np.int32)
+    _full_check(cfg, 0, P.PREFIX_SUMMARY, sel, q, k, v)
+    _full_check(cfg, 1, P.PREFIX_SUMMARY, sel, q, k, v)

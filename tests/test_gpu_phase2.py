@@ -108,3 +108,17 @@ def test_tiny_phase2_one_query_over_four_shards():
     torch.cuda.synchronize()
     ref = attention.dense_attention(f64(q), f64(k_all[0]), f64(v_all[0]), 1 / math.sqrt(cfg.d))
     check_attention(o.cpu().numpy(), lse.cpu().numpy(), *ref, "tiny phase 2")
+
+
+def test_phase2_far_larger_later_score():
+    Tq, Hq, Hkv, d, S = 8, 8, 2, 128, 700
+    q = workload.bf16_bits_to_f32(workload.bf16_normal(3, (Tq, Hq, d))) + 1.0
+    kf = workload.bf16_bits_to_f32(workload.bf16_normal(4, (2, S, Hkv, d)))
+    kf[1, 300] = 8.0
+    qb, kb = workload.f32_to_bf16_bits(q), workload.f32_to_bf16_bits(kf)
+    vb = workload.bf16_normal(5, (2, S, Hkv, d))
+    o_parts, lse_parts = P.phase2_partial(to_dev_bf16(qb), to_dev_bf16(kb), to_dev_bf16(vb))
+    torch.cuda.synchronize()
+    for h in range(2):
+        ref = attention.partial_attention(f64(qb), f64(kb[h]), f64(vb[h]), 1 / math.sqrt(d))
+        check_attention(o_parts[h].cpu().numpy(), lse_parts[h].cpu().numpy(), *ref, f"shard {h}")
