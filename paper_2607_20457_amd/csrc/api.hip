@@ -34,21 +34,18 @@ RowMap make_map(int64_t L, int num_blocks, int block_idx, int sink, int chunk, i
   mp.sink = sink;
   mp.chunk = chunk;
   mp.topk = topk;
-  mp.sigma = topk * chunk;
-  mp.inv_sigma = mp.sigma > 0 ? 1.0f / (float)mp.sigma : 0.f;
-  mp.inv_chunk = 1.0f / (float)chunk;
   mp.nchunk = Lb / chunk;
+  mp.m_log2 = is_pow2(chunk) ? __builtin_ctz(chunk) : -1;
+  mp.inv_chunk = 1.0f / (float)chunk;
   if (block_idx == 0) {
     mp.mode = MAP_IDENTITY;
     mp.offset = 0;
   } else if (prefix_mode == PULSAR_PREFIX_ANCHOR) {
     mp.mode = MAP_ANCHOR;
-  } else if (topk == 0) {
-    mp.mode = MAP_SUMMARY;
-    mp.prefix = 0;
   } else {
     mp.mode = MAP_SUMMARY;
-    mp.prefix = block_idx * mp.sigma;
+    mp.n_runs = block_idx * topk;
+    mp.prefix = mp.n_runs * chunk;
   }
   return mp;
 }
@@ -108,6 +105,7 @@ int pulsar_phase1_positions(const int32_t* sel_chunks, int batch, int64_t L, int
   const int64_t n = phase1_len_checked(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
   if (n < 0) return (int)n;
   if (batch < 0 || L >= ((int64_t)1 << 31)) return PULSAR_EINVAL;
+  if (n >= PULSAR_MAX_ROWS) return PULSAR_EUNSUPPORTED;
   if (batch == 0 || n == 0) return PULSAR_OK;
   if (pos == nullptr) return PULSAR_EINVAL;
   if (needs_sel(block_idx, topk, prefix_mode) && sel_chunks == nullptr) return PULSAR_EINVAL;
@@ -131,6 +129,7 @@ int pulsar_phase1_attn(const void* Q, const void* K, const void* V, int batch, i
   if ((K_keep == nullptr) != (V_keep == nullptr)) return PULSAR_EINVAL;
   if (d != 64 && d != 128) return PULSAR_EUNSUPPORTED;
   if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
+  if (n >= PULSAR_MAX_ROWS || L * Hkv * d * 2 >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
   if (batch == 0 || n == 0) return PULSAR_OK;
   if (Q == nullptr || K == nullptr || V == nullptr || O == nullptr) return PULSAR_EINVAL;
   if (needs_sel(block_idx, topk, prefix_mode) && sel_chunks == nullptr) return PULSAR_EINVAL;
@@ -216,7 +215,9 @@ int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_sha
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale)) return PULSAR_EINVAL;
   if (d != 64 && d != 128) return PULSAR_EUNSUPPORTED;
   if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
-  if (S >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
+  if (S >= ((int64_t)1 << 31) || S * Hkv * d * 2 >= ((int64_t)1 << 31) ||
+      Tq >= PULSAR_MAX_ROWS)
+    return PULSAR_EUNSUPPORTED;
   if (n_shards == 0 || Tq == 0) return PULSAR_OK;
   if (q == nullptr || o_parts == nullptr || lse_parts == nullptr) return PULSAR_EINVAL;
   if (S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;

@@ -43,6 +43,7 @@ constexpr int BN = 64;          // keys per tile
 constexpr int THREADS = 256;    // 4 wavefronts
 constexpr float MAX_SLACK = 8.0f;  // exact pass: log2 slack before the running max is raised
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer access (word 3 of the resource)
 __device__ constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 
 template <int D>
@@ -127,13 +128,28 @@ void attn_fwd_kernel(KernelArgs ka) {
 
   uint8_t* stage0 = smem;
   int32_t* lpos = reinterpret_cast<int32_t*>(smem + 2 * T::STAGE);  // [2][BN]
+  int* run_base = lpos + 2 * BN;                                      // [map.n_runs]
+  build_run_table(a.map, sel, run_base, tid, THREADS);
+  __syncthreads();
+
+  // K/V rows are read through buffer resources covering this sequence (or
+  // shard); a padded key has position -1, whose offset falls outside the
+  // resource, so the hardware returns zeros for it.
+  const uint32_t row_bytes = (uint32_t)(a.Hkv * D * 2);
+  const __amdgpu_buffer_rsrc_t k_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.K + zkv * a.kv_zstride), (short)0, (int)(a.kv_zstride * 2),
+      kBufferFlags);
+  const __amdgpu_buffer_rsrc_t v_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.V + zkv * a.kv_zstride), (short)0, (int)(a.kv_zstride * 2),
+      kBufferFlags);
+  const uint32_t head_off = (uint32_t)(kvh * D * 2);
 
   // ---- Q fragments (B operand of S^T = K Q^T) --------------------------------
   bf16x8 qf[QT][DS];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     const int r = row0 + t * 32 + l32;
-    const int p = r < a.n_q ? row_position(a.map, sel, r) : 0;
+    const int p = r < a.n_q ? row_position(a.map, run_base, r) : 0;
     const bf16x8* src = reinterpret_cast<const bf16x8*>(Qz + (int64_t)p * q_row) + g;
 #pragma unroll
     for (int s = 0; s < DS; ++s) qf[t][s] = r < a.n_q ? src[2 * s] : bf16x8{};
@@ -151,12 +167,11 @@ void attn_fwd_kernel(KernelArgs ka) {
   auto tile_positions = [&](int j, int32_t* dst) {
     if (tid < BN) {
       const int k = kv_begin + j * BN + tid;
-      dst[tid] = k < kv_end ? row_position(a.map, sel, k) : -1;
+      dst[tid] = k < kv_end ? row_position(a.map, run_base, k) : -1;
     }
   };
   u32x4 kreg[KR];
   u32x4 vreg[4];
-  int vpos[4];  // kept to zero the V rows of padded keys when they are stored
   const bool v_thread = tid < T::V_UNITS;
   auto load_regs = [&](const int32_t* pos) {
     const int kr0 = KR * (tid / T::CPR);
@@ -168,17 +183,19 @@ void attn_fwd_kernel(KernelArgs ka) {
 #pragma unroll
       for (int i = 0; i < KR; ++i) kp[i] = pos[kr0 + i];
     }
+    const uint32_t kcol = head_off + (uint32_t)(tid % T::CPR) * 16;
 #pragma unroll
     for (int i = 0; i < KR; ++i)
-      kreg[i] = *reinterpret_cast<const u32x4*>(Kz + (int64_t)max(kp[i], 0) * kv_row +
-                                                (tid % T::CPR) * 8);
+      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(k_rsrc, (int)((uint32_t)kp[i] * row_bytes + kcol),
+                                                      0, 0);
     if (v_thread) {
       const int4 p4 = *reinterpret_cast<const int4*>(pos + 4 * (tid & 15));
-      vpos[0] = p4.x; vpos[1] = p4.y; vpos[2] = p4.z; vpos[3] = p4.w;
-      const int dc = tid >> 4;
+      const int vp[4] = {p4.x, p4.y, p4.z, p4.w};
+      const uint32_t vcol = head_off + (uint32_t)(tid >> 4) * 16;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr)
-        vreg[rr] = *reinterpret_cast<const u32x4*>(Vz + (int64_t)max(vpos[rr], 0) * kv_row + dc * 8);
+        vreg[rr] = __builtin_amdgcn_raw_buffer_load_b128(
+            v_rsrc, (int)((uint32_t)vp[rr] * row_bytes + vcol), 0, 0);
     }
   };
   auto store_lds = [&](uint8_t* st) {
@@ -188,11 +205,6 @@ void attn_fwd_kernel(KernelArgs ka) {
       *reinterpret_cast<u32x4*>(st + swap_bits23(kr0 + i) * T::K_STRIDE + (tid % T::CPR) * 16) =
           kreg[i];
     if (v_thread) {
-      // rows past the end become zero, so that a zero weight never meets a
-      // non-finite value
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        if (vpos[rr] < 0) vreg[rr] = u32x4{0u, 0u, 0u, 0u};
       uint8_t* sv = st + T::K_BYTES;
       const int kq = tid & 15;
       const int dc = tid >> 4;
@@ -378,11 +390,13 @@ int launch_impl(const KernelArgs& ka, hipStream_t stream) {
   const int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
   if (nwg == 0) return PULSAR_OK;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
+  const int64_t lds = Tile<D>::LDS + (int64_t)ka.a.map.n_runs * 4;
+  if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
   auto kern = attn_fwd_kernel<D, QT, CAUSAL>;
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          Tile<D>::LDS) != hipSuccess)
+                          (int)lds) != hipSuccess)
     return PULSAR_EHIP;
-  hipLaunchKernelGGL(kern, dim3((unsigned)nwg), dim3(THREADS), Tile<D>::LDS, stream, ka);
+  hipLaunchKernelGGL(kern, dim3((unsigned)nwg), dim3(THREADS), (size_t)lds, stream, ka);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
 

@@ -17,7 +17,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define PULSAR_WAVE 64
 #define PULSAR_LDS_BYTES 163840  // 160 KB local data share per compute unit on gfx950
 
-// Row -> global position map of an attention launch.
+// Row -> global position map of an assembled Phase-1 input (Eq. 3, sparse
+// position ids).  The summary region is a sequence of runs of m consecutive
+// positions, one run per selected chunk; run q = j*k + c starts at
+// j*Lb + sel[j][c]*m.  Kernels stage these run starts in LDS once
+// (build_run_table) and then map a row with a few integer operations.
 enum MapMode : int { MAP_IDENTITY = 0, MAP_SUMMARY = 1, MAP_ANCHOR = 2 };
 
 struct RowMap {
@@ -27,44 +31,50 @@ struct RowMap {
   int sink;        // s_sink
   int chunk;       // m
   int topk;        // k
-  int sigma;       // k * m
-  int prefix;      // summary rows = i * sigma (summary mode)
+  int prefix;      // rows of the summary region, i * k * m (summary mode)
+  int n_runs;      // summary runs, i * k
   int nchunk;      // chunks per block, Lb / m
+  int m_log2;      // log2(m) when m is a power of two, else -1
+  float inv_chunk; // 1 / m
   int64_t offset;  // identity mode: position of row 0
-  float inv_sigma; // 1 / sigma, for the quotient estimate below
-  float inv_chunk; // 1 / chunk
 };
 
-// Quotient of two non-negative ints through a float estimate and an exact
-// correction step (the estimate is off by at most one below 2^24).
-__device__ __forceinline__ int div_fix(int a, int b, float inv_b, int* rem) {
-  int q = (int)((float)a * inv_b);
-  int r = a - q * b;
-  while (r < 0) { --q; r += b; }
-  while (r >= b) { ++q; r -= b; }
-  *rem = r;
-  return q;
+// run_base[q] = j*Lb + sel[j][c]*m for run q = j*k + c; a selection outside
+// [0, Lb/m) is a caller error and is clamped so that every access stays
+// inside block j.
+__device__ __forceinline__ void build_run_table(const RowMap& mp, const int32_t* __restrict__ sel,
+                                                int* run_base, int tid, int nthreads) {
+  for (int q = tid; q < mp.n_runs; q += nthreads) {
+    const int j = q / mp.topk;
+    const int c = min(max(sel[q], 0), mp.nchunk - 1);
+    run_base[q] = j * mp.Lb + c * mp.chunk;
+  }
 }
 
-// Global position of assembled row r (Eq. 3, sparse position ids).
-// sel points at this sequence's [num_blocks, topk] selection.
-__device__ __forceinline__ int row_position(const RowMap& mp, const int32_t* __restrict__ sel,
-                                            int r) {
+// Global position of assembled row r.  Rows are below 2^24 (checked on the
+// host), so the float quotient estimate is within one of the true quotient.
+__device__ __forceinline__ int row_position(const RowMap& mp, const int* run_base, int r) {
   if (mp.mode == MAP_IDENTITY) return (int)(mp.offset + r);
   if (mp.mode == MAP_ANCHOR) return r < mp.Lb ? r : mp.block_idx * mp.Lb + (r - mp.Lb);
   if (r < mp.sink) return r;
-  int t = r - mp.sink;
-  if (t < mp.prefix) {
-    int w;
-    int j = div_fix(t, mp.sigma, mp.inv_sigma, &w);
-    int rr;
-    int c = div_fix(w, mp.chunk, mp.inv_chunk, &rr);
-    // a selection outside [0, Lb/m) is a caller error; clamping keeps every
-    // access inside block j
-    const int cs = min(max(sel[j * mp.topk + c], 0), mp.nchunk - 1);
-    return j * mp.Lb + cs * mp.chunk + rr;
+  const int t = r - mp.sink;
+  if (t >= mp.prefix) return mp.block_idx * mp.Lb + (t - mp.prefix);
+  int q, w;
+  if (mp.m_log2 >= 0) {
+    q = t >> mp.m_log2;
+    w = t & (mp.chunk - 1);
+  } else {
+    q = (int)((float)t * mp.inv_chunk);
+    w = t - q * mp.chunk;
+    if (w < 0) {
+      --q;
+      w += mp.chunk;
+    } else if (w >= mp.chunk) {
+      ++q;
+      w -= mp.chunk;
+    }
   }
-  return mp.block_idx * mp.Lb + (t - mp.prefix);
+  return run_base[q] + w;
 }
 
 __device__ __forceinline__ float wave_max(float x) {
@@ -99,6 +109,7 @@ size_t maxidf_lds_bytes(int64_t L, int chunk, int vocab);
 
 int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
                      int n_rows, int32_t* pos, hipStream_t stream);
+#define PULSAR_MAX_ROWS (1 << 24)  // longest assembled input the row map supports
 
 struct AttnLaunch {
   const uint16_t* Q;

@@ -3,21 +3,30 @@
 #include "common.hpp"
 
 // ---------------------------------------------------------------------------
-// Row -> global position map (Eq. 3, sparse position ids).
+// Row -> global position map (Eq. 3, sparse position ids), with the same
+// device function the attention kernel uses for its fused gather.
 __global__ __launch_bounds__(256) void positions_kernel(RowMap mp, const int32_t* __restrict__ sel,
                                                         int64_t sel_bstride, int n_rows,
                                                         int32_t* __restrict__ pos) {
+  extern __shared__ int run_base[];
   const int b = blockIdx.y;
+  build_run_table(mp, sel ? sel + b * sel_bstride : nullptr, run_base, threadIdx.x, 256);
+  __syncthreads();
   const int r = blockIdx.x * 256 + threadIdx.x;
   if (r >= n_rows) return;
-  pos[(int64_t)b * n_rows + r] = row_position(mp, sel ? sel + b * sel_bstride : nullptr, r);
+  pos[(int64_t)b * n_rows + r] = row_position(mp, run_base, r);
 }
 
 int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
                      int n_rows, int32_t* pos, hipStream_t stream) {
   if (batch == 0 || n_rows == 0) return PULSAR_OK;
+  const size_t lds = (size_t)mp.n_runs * 4;
+  if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
+  if (hipFuncSetAttribute((const void*)positions_kernel,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return PULSAR_EHIP;
   dim3 grid((n_rows + 255) / 256, batch);
-  hipLaunchKernelGGL(positions_kernel, grid, dim3(256), 0, stream, mp, sel, sel_bstride, n_rows,
+  hipLaunchKernelGGL(positions_kernel, grid, dim3(256), lds, stream, mp, sel, sel_bstride, n_rows,
                      pos);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
