@@ -86,10 +86,18 @@ def gather_rows(x, pos):
 
 def phase1_attention(Q, K, V, pos, scale: float, rows=None):
     """Phase-1 attention for one sequence over the assembled input whose rows
-    copy the global positions ``pos``.  Q [L, Hq, d], K/V [L, Hkv, d]."""
-    q, k, v = gather_rows(Q, pos), gather_rows(K, pos), gather_rows(V, pos)
+    copy the global positions ``pos``.  Q [L, Hq, d], K/V [L, Hkv, d].
+    With ``rows`` only those assembled rows are computed (and only the rows
+    they can see are gathered)."""
+    pos = np.asarray(pos, dtype=np.int64)
     if rows is None:
+        q, k, v = gather_rows(Q, pos), gather_rows(K, pos), gather_rows(V, pos)
         return causal_attention(q, k, v, scale)
+    rows = np.asarray(rows, dtype=np.int64)
+    last = int(rows.max()) + 1
+    k, v = gather_rows(K, pos[:last]), gather_rows(V, pos[:last])
+    q = np.zeros((last,) + np.shape(Q)[1:])
+    q[rows] = gather_rows(Q, pos[rows])
     return causal_attention_rows(q, k, v, scale, rows)
 
 
