@@ -79,7 +79,7 @@ __device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
   return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-template <int D, int QT, bool CAUSAL>
+template <int D, int QT, bool CAUSAL, bool LSE>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(3 - QT, 3 - QT)))
 void attn_fwd_kernel(KernelArgs ka) {
   using T = Tile<D>;
@@ -221,16 +221,78 @@ void attn_fwd_kernel(KernelArgs ka) {
     }
   };
 
-  // ---- one pass over all key tiles ------------------------------------------
-  // EXACT = false: every row's scores are taken relative to a fixed reference
-  //   (the maximum over the first 32 keys), so the accumulator is never
-  //   rescaled.  A weight above 2^64 flags the pass as unsafe.
-  // EXACT = true: classic online softmax that raises the running maximum when
-  //   it grows by more than 2^8 and rescales the accumulator; it runs only
-  //   for workgroups whose first pass was flagged.
-  auto pass = [&](auto exact_tag) -> bool {
-    constexpr bool EXACT = decltype(exact_tag)::value;
-    bool overflow = false;
+  // ---- building blocks of one 32-key half --------------------------------------
+  // S^T of keys u*32..u*32+31 of the tile in LDS against this wave's queries.
+  auto s_product = [&](const uint8_t* sK, int u, f32x16 (&S)[QT]) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) S[t] = f32x16{};
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
+                                                         (16 * s + 8 * g) * 2);
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+        S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[t], 0, 0, 0);
+    }
+  };
+  // -inf for keys after the query row (causal) or past the last key.
+  auto apply_mask = [&](int kh, f32x16 (&S)[QT]) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int qrow = row0 + t * 32 + l32;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = kh + 16 * (v >> 3) + 8 * g + (v & 7);
+        const bool masked = CAUSAL ? (key > qrow || key >= kv_end) : (key >= kv_end);
+        if (masked) S[t][v] = -INFINITY;
+      }
+    }
+  };
+  auto row_max = [&](const f32x16& S) {
+    float mx = S[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, S[v]);
+    return fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;  // both lanes of a query agree
+  };
+  // Weights relative to m_ref, their bf16-rounded sum (which normalises O),
+  // the fp32 sum when the LSE is wanted, and P in the B-operand layout of the
+  // PV product.
+  auto weights = [&](const f32x16 (&S)[QT], bf16x8 (&pf)[2][QT]) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float psum = 0.f;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        f32x8 p;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[t][8 * c + v], c2, -m_ref[t]));
+          if (LSE) psum += p[v];
+        }
+        pf[c][t] = __builtin_convertvector(p, bf16x8);
+        const bf16x8 w = pf[c][t];
+#pragma unroll
+        for (int v = 0; v < 8; v += 2)
+          lr_run[t] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[v], w[v + 1]}, kOnes2, lr_run[t],
+                                                      false);
+      }
+      if (LSE) l_run[t] += psum;
+    }
+  };
+  auto pv_product = [&](const uint8_t* sV, int u, const bf16x8 (&pf)[2][QT]) {
+#pragma unroll
+    for (int e = 0; e < DT; ++e)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+            sV + (e * 32 + l32) * T::V_STRIDE + (u * 32 + 16 * c + 8 * g) * 2);
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c][t], acc[e][t], 0, 0, 0);
+      }
+  };
+
+  auto reset = [&]() {
 #pragma unroll
     for (int e = 0; e < DT; ++e)
 #pragma unroll
@@ -241,116 +303,95 @@ void attn_fwd_kernel(KernelArgs ka) {
       l_run[t] = 0.f;
       lr_run[t] = 0.f;
     }
-    if (ntiles > 0) {
-      tile_positions(0, lpos);
-      __syncthreads();
-      if (ntiles > 1) tile_positions(1, lpos + BN);
-      load_regs(lpos);
-      store_lds(stage0);
-    }
+  };
+  // Tile 0 written to stage 0 and tile 1's positions staged.
+  auto prologue = [&]() {
+    tile_positions(0, lpos);
+    __syncthreads();
+    if (ntiles > 1) tile_positions(1, lpos + BN);
+    load_regs(lpos);
+    store_lds(stage0);
+  };
+  // Iteration j: wait for tile j in LDS, prefetch tile j+1 into registers, run
+  // `body`, then store tile j+1 into the other buffer.
+  auto tile_loop = [&](auto&& body) {
     for (int j = 0; j < ntiles; ++j) {
       __syncthreads();
       const int buf = j & 1;
-      if (j + 1 < ntiles) load_regs(lpos + ((j + 1) & 1) * BN);
+      if (j + 1 < ntiles) load_regs(lpos + (buf ^ 1) * BN);
       if (j + 2 < ntiles) tile_positions(j + 2, lpos + buf * BN);
-
-      const int kbase = kv_begin + j * BN;
       const uint8_t* sK = stage0 + buf * T::STAGE;
-      const uint8_t* sV = sK + T::K_BYTES;
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int kh = kbase + 32 * u;  // first key of this 32-key half
-        if (CAUSAL && kh > row0 + QR - 1) continue;  // all masked for this wave
-        f32x16 S[QT];
-#pragma unroll
-        for (int t = 0; t < QT; ++t) S[t] = f32x16{};
-#pragma unroll
-        for (int s = 0; s < DS; ++s) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
-                                                             (16 * s + 8 * g) * 2);
-#pragma unroll
-          for (int t = 0; t < QT; ++t)
-            S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[t], 0, 0, 0);
-        }
-
-        const bool edge = CAUSAL ? (kh + 31 > row0) : (kh + 32 > kv_end);
-        if (edge) {
-#pragma unroll
-          for (int t = 0; t < QT; ++t) {
-            const int qrow = row0 + t * 32 + l32;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const int key = kh + 16 * (v >> 3) + 8 * g + (v & 7);
-              const bool masked = CAUSAL ? (key > qrow || key >= kv_end) : (key >= kv_end);
-              if (masked) S[t][v] = -INFINITY;
-            }
-          }
-        }
-        const bool first = j == 0 && u == 0;
-        bf16x8 pf[2][QT];
-#pragma unroll
-        for (int t = 0; t < QT; ++t) {
-          if (EXACT || first) {
-            float mx = S[t][0];
-#pragma unroll
-            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, S[t][v]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
-            if (!EXACT) {
-              m_ref[t] = mx;
-            } else {
-              const bool raise = mx > m_ref[t] + MAX_SLACK;
-              const float m_use = raise ? mx : m_ref[t];
-              if (__any(raise)) {
-                const float alpha = __builtin_amdgcn_exp2f(m_ref[t] - m_use);
-#pragma unroll
-                for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
-                l_run[t] *= alpha;
-                lr_run[t] *= alpha;
-              }
-              m_ref[t] = m_use;
-            }
-          }
-          float psum = 0.f;
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            f32x8 p;
-#pragma unroll
-            for (int v = 0; v < 8; ++v) {
-              p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[t][8 * c + v], c2, -m_ref[t]));
-              psum += p[v];
-            }
-            pf[c][t] = __builtin_convertvector(p, bf16x8);
-            const bf16x8 w = pf[c][t];
-#pragma unroll
-            for (int v = 0; v < 8; v += 2)
-              lr_run[t] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{w[v], w[v + 1]}, kOnes2,
-                                                          lr_run[t], false);
-          }
-          l_run[t] += psum;
-          if (!EXACT) overflow |= !(psum <= 0x1p64f);  // also true for inf
-        }
-
-#pragma unroll
-        for (int e = 0; e < DT; ++e)
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-                sV + (e * 32 + l32) * T::V_STRIDE + (u * 32 + 16 * c + 8 * g) * 2);
-#pragma unroll
-            for (int t = 0; t < QT; ++t)
-              acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c][t], acc[e][t], 0, 0, 0);
-          }
-      }
-
+      body(kv_begin + j * BN, sK, sK + T::K_BYTES);
       if (j + 1 < ntiles) store_lds(stage0 + (buf ^ 1) * T::STAGE);
     }
-    return overflow;
   };
 
-  const bool ovf = pass(std::false_type{});
-  if (__syncthreads_or(ovf)) {
+  // ---- fast pass: fixed per-row reference, O touched only by MFMA -----------
+  // The reference is the row's maximum over the first 32 keys; only halves
+  // that reach past a query row (or past the last key) are masked.
+  bool overflow = false;
+  reset();
+  if (ntiles > 0) {
+    prologue();
     __syncthreads();
-    pass(std::true_type{});
+    f32x16 S[QT];
+    s_product(stage0, 0, S);
+    apply_mask(kv_begin, S);
+#pragma unroll
+    for (int t = 0; t < QT; ++t) m_ref[t] = row_max(S[t]);
+  }
+  tile_loop([&](int kbase, const uint8_t* sK, const uint8_t* sV) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int kh = kbase + 32 * u;
+      if (CAUSAL && kh > row0 + QR - 1) continue;  // every key after every row
+      f32x16 S[QT];
+      bf16x8 pf[2][QT];
+      s_product(sK, u, S);
+      if (CAUSAL ? (kh + 31 > row0) : (kh + 32 > kv_end)) apply_mask(kh, S);
+      weights(S, pf);
+      pv_product(sV, u, pf);
+    }
+  });
+  // Every weight is at most the final sum, so a finite sum below 2^88 bounds
+  // them all; above that (or not finite) the exact pass takes over.
+#pragma unroll
+  for (int t = 0; t < QT; ++t) overflow |= !(lr_run[t] <= 0x1p88f);
+
+  // ---- exact pass: classic online softmax, only after an overflow flag --------
+  // The running maximum is raised when a half's maximum exceeds it by more
+  // than 2^8, and O and the sums are rescaled.
+  if (__syncthreads_or(overflow)) {
+    __syncthreads();
+    reset();
+    if (ntiles > 0) prologue();
+    tile_loop([&](int kbase, const uint8_t* sK, const uint8_t* sV) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int kh = kbase + 32 * u;
+        if (CAUSAL && kh > row0 + QR - 1) continue;
+        f32x16 S[QT];
+        bf16x8 pf[2][QT];
+        s_product(sK, u, S);
+        apply_mask(kh, S);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) {
+          const float mx = row_max(S[t]);
+          const bool raise = mx > m_ref[t] + MAX_SLACK;
+          const float m_use = raise ? mx : m_ref[t];
+          if (__any(raise)) {
+            const float alpha = __builtin_amdgcn_exp2f(m_ref[t] - m_use);
+#pragma unroll
+            for (int e = 0; e < DT; ++e) acc[e][t] *= alpha;
+            l_run[t] *= alpha;
+            lr_run[t] *= alpha;
+          }
+          m_ref[t] = m_use;
+        }
+        weights(S, pf);
+        pv_product(sV, u, pf);
+      }
+    });
   }
 
   // ---- epilogue: normalise, write O and LSE ---------------------------------
@@ -376,7 +417,7 @@ void attn_fwd_kernel(KernelArgs ka) {
             *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.O) + obase + dd) = o4;
           }
         }
-      if (a.lse && g == 0) {
+      if (LSE && g == 0) {
         const float lse = l_tot > 0.f ? (m_ref[t] + __log2f(l_tot)) * 0.69314718055994531f
                                       : -INFINITY;
         a.lse[(int64_t)z * a.lse_zstride + (int64_t)head * a.n_q + qrow] = lse;
@@ -385,14 +426,14 @@ void attn_fwd_kernel(KernelArgs ka) {
   }
 }
 
-template <int D, int QT, bool CAUSAL>
+template <int D, int QT, bool CAUSAL, bool LSE>
 int launch_impl(const KernelArgs& ka, hipStream_t stream) {
   const int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
   if (nwg == 0) return PULSAR_OK;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const int64_t lds = Tile<D>::LDS + (int64_t)ka.a.map.n_runs * 4;
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
-  auto kern = attn_fwd_kernel<D, QT, CAUSAL>;
+  auto kern = attn_fwd_kernel<D, QT, CAUSAL, LSE>;
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds) != hipSuccess)
     return PULSAR_EHIP;
@@ -424,9 +465,17 @@ int launch_attention(const AttnLaunch& a, hipStream_t stream) {
   ka.rows_per_wg = attn_rows_per_wg(ka.group);
   ka.n_row_tiles = (a.n_q + ka.rows_per_wg - 1) / ka.rows_per_wg;
   ka.nz = a.nz_kv * a.nsplit;
+  const bool lse = a.lse != nullptr;
   if (a.d == 128) {
-    return a.causal ? launch_impl<128, kQT, true>(ka, stream)
-                    : launch_impl<128, kQT, false>(ka, stream);
+    if (a.causal)
+      return lse ? launch_impl<128, kQT, true, true>(ka, stream)
+                 : launch_impl<128, kQT, true, false>(ka, stream);
+    return lse ? launch_impl<128, kQT, false, true>(ka, stream)
+               : launch_impl<128, kQT, false, false>(ka, stream);
   }
-  return a.causal ? launch_impl<64, kQT, true>(ka, stream) : launch_impl<64, kQT, false>(ka, stream);
+  if (a.causal)
+    return lse ? launch_impl<64, kQT, true, true>(ka, stream)
+               : launch_impl<64, kQT, true, false>(ka, stream);
+  return lse ? launch_impl<64, kQT, false, true>(ka, stream)
+             : launch_impl<64, kQT, false, false>(ka, stream);
 }
