@@ -114,7 +114,7 @@ def cpu_oracle_baseline(ids, q, k, v, sel_ref, cfg, n, budget_s=15.0):
     f64 = lambda x: workload.bf16_bits_to_f32(x).astype(np.float64)
     Q, K, V = f64(q[0]), f64(k[0]), f64(v[0])
     scale = 1 / math.sqrt(cfg.d)
-    rows_all = np.linspace(0, n - 1, 256).astype(np.int64)[::-1]   # longest rows first
+    rows_all = np.linspace(0, n - 1, 2048).astype(np.int64)[::-1]  # longest rows first
     flops, done, t_attn = 0, 0, 0.0
     for b0 in range(0, rows_all.size, 8):
         rows = rows_all[b0:b0 + 8]
@@ -160,8 +160,10 @@ def run_main(args):
         with (t_idf if timed else _Null()):
             sel = P.maxidf_summaries(d_ids, N, cfg.chunk, cfg.topk, cfg.vocab)
         with (t_p1 if timed else _Null()):
-            _, lse, Kk, Vk = P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, sel,
-                                           out=O, keep_kv=True)
+            # the forward pass yields O for every row and the retained KV(B_15);
+            # no LSE is needed downstream of Phase 1
+            P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, sel, out=O,
+                          return_lse=False, keep_kv=True)
         with (t_p2 if timed else _Null()):
             shards_k = K[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
             shards_v = V[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
@@ -243,6 +245,16 @@ def run_main(args):
             "traffic": measured_traffic("attn_phase1_128k_block15"),
         },
     }
+    if args.calibrate:
+        # a plain device copy of a known size (1 GiB read, 1 GiB write), far
+        # larger than the caches: the scale for the FETCH_SIZE / WRITE_SIZE
+        # counters of a rocprofv3 --pmc run of this command
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["calibration_copy_bytes"] = src.numel() * 4
     if not args.no_cpu:
         from oracle import maxidf as oracle_maxidf
         sel_ref, _, _, _ = oracle_maxidf.maxidf_summaries(ids, N, cfg.chunk, cfg.topk, cfg.vocab)
@@ -344,6 +356,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="append a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the library runs on a single GPU and has "
