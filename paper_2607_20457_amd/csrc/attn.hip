@@ -6,10 +6,11 @@
 //    split along the keys, giving (o, lse) partials (Algorithm 1, Phase 2).
 //
 // Work decomposition
-//   A workgroup is 4 wavefronts.  All of them read the same KV head; when the
-//   group size Hq/Hkv is a multiple of 4 the waves are 4 query heads of that
-//   group over the same 32*QT rows (grouped-query sharing: one K/V tile in
-//   LDS feeds four heads), otherwise the waves also split the rows.
+//   A workgroup is 8 wavefronts (2 per SIMD), all reading the same
+//   KV head.  When the group size Hq/Hkv is a multiple of 4, four consecutive
+//   waves are 4 query heads of that group over the same 32*QT rows
+//   (grouped-query sharing: one K/V tile in LDS feeds four heads); further
+//   waves, or smaller groups, split the rows.
 //   Workgroup ids run heaviest causal row tile first, and the KV head is the
 //   fastest-varying index, so with 8 KV heads each XCD's L2 serves one head.
 //
@@ -40,7 +41,6 @@
 namespace {
 
 constexpr int BN = 64;          // keys per tile
-constexpr int THREADS = 256;    // 4 wavefronts
 constexpr float MAX_SLACK = 8.0f;  // exact pass: log2 slack before the running max is raised
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer access (word 3 of the resource)
@@ -55,7 +55,7 @@ struct Tile {
   static constexpr int STAGE = K_BYTES + V_BYTES;
   static constexpr int LDS = 2 * STAGE + 2 * BN * 4;  // two stages + two position rows
   static constexpr int CPR = D / 8;               // 16-byte chunks per row
-  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= THREADS)
+  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= threads)
 };
 
 struct KernelArgs {
@@ -79,9 +79,10 @@ __device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
   return (a >> 16) | (b & 0xFFFF0000u);
 }
 
-template <int D, int QT, bool CAUSAL, bool LSE>
-__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(3 - QT, 3 - QT)))
+template <int D, int QT, int WAVES, bool CAUSAL, bool LSE>
+__global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(3 - QT, 3 - QT)))
 void attn_fwd_kernel(KernelArgs ka) {
+  constexpr int THREADS = 64 * WAVES;
   using T = Tile<D>;
   constexpr int QR = 32 * QT;        // rows per wavefront
   constexpr int DS = D / 16;         // k-steps of the S product
@@ -426,18 +427,18 @@ void attn_fwd_kernel(KernelArgs ka) {
   }
 }
 
-template <int D, int QT, bool CAUSAL, bool LSE>
+template <int D, int QT, int WAVES, bool CAUSAL, bool LSE>
 int launch_impl(const KernelArgs& ka, hipStream_t stream) {
   const int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
   if (nwg == 0) return PULSAR_OK;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const int64_t lds = Tile<D>::LDS + (int64_t)ka.a.map.n_runs * 4;
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
-  auto kern = attn_fwd_kernel<D, QT, CAUSAL, LSE>;
+  auto kern = attn_fwd_kernel<D, QT, WAVES, CAUSAL, LSE>;
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds) != hipSuccess)
     return PULSAR_EHIP;
-  hipLaunchKernelGGL(kern, dim3((unsigned)nwg), dim3(THREADS), (size_t)lds, stream, ka);
+  hipLaunchKernelGGL(kern, dim3((unsigned)nwg), dim3(64 * WAVES), (size_t)lds, stream, ka);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
 
@@ -451,9 +452,20 @@ int launch_impl(const KernelArgs& ka, hipStream_t stream) {
 #endif
 constexpr int kQT = PULSAR_ATTN_QT;
 
-int attn_rows_per_wg(int group) {
+// Wavefronts per workgroup: 8, i.e. two 32-row groups of four heads, so that
+// one K/V tile in LDS serves 64 rows of four heads (for Phase 2: all 64
+// queries); the two wavefronts that share a SIMD interleave their matrix and
+// vector work.
+#ifndef PULSAR_CAUSAL_WAVES
+#define PULSAR_CAUSAL_WAVES 8
+#endif
+constexpr int kCausalWaves = PULSAR_CAUSAL_WAVES;
+constexpr int kPartialWaves = 8;
+
+int attn_rows_per_wg(int group, bool causal) {
   const int heads_per_wg = group >= 4 ? 4 : group;
-  return 32 * kQT * (4 / heads_per_wg);
+  const int waves = causal ? kCausalWaves : kPartialWaves;
+  return 32 * kQT * (waves / heads_per_wg);
 }
 
 int launch_attention(const AttnLaunch& a, hipStream_t stream) {
@@ -462,20 +474,21 @@ int launch_attention(const AttnLaunch& a, hipStream_t stream) {
   ka.group = a.Hq / a.Hkv;
   ka.heads_per_wg = ka.group >= 4 ? 4 : ka.group;
   ka.hsub = ka.group / ka.heads_per_wg;
-  ka.rows_per_wg = attn_rows_per_wg(ka.group);
+  ka.rows_per_wg = attn_rows_per_wg(ka.group, a.causal != 0);
   ka.n_row_tiles = (a.n_q + ka.rows_per_wg - 1) / ka.rows_per_wg;
   ka.nz = a.nz_kv * a.nsplit;
   const bool lse = a.lse != nullptr;
+  constexpr int CW = kCausalWaves, PW = kPartialWaves;
   if (a.d == 128) {
     if (a.causal)
-      return lse ? launch_impl<128, kQT, true, true>(ka, stream)
-                 : launch_impl<128, kQT, true, false>(ka, stream);
-    return lse ? launch_impl<128, kQT, false, true>(ka, stream)
-               : launch_impl<128, kQT, false, false>(ka, stream);
+      return lse ? launch_impl<128, kQT, CW, true, true>(ka, stream)
+                 : launch_impl<128, kQT, CW, true, false>(ka, stream);
+    return lse ? launch_impl<128, kQT, PW, false, true>(ka, stream)
+               : launch_impl<128, kQT, PW, false, false>(ka, stream);
   }
   if (a.causal)
-    return lse ? launch_impl<64, kQT, true, true>(ka, stream)
-               : launch_impl<64, kQT, true, false>(ka, stream);
-  return lse ? launch_impl<64, kQT, false, true>(ka, stream)
-             : launch_impl<64, kQT, false, false>(ka, stream);
+    return lse ? launch_impl<64, kQT, CW, true, true>(ka, stream)
+               : launch_impl<64, kQT, CW, true, false>(ka, stream);
+  return lse ? launch_impl<64, kQT, PW, false, true>(ka, stream)
+             : launch_impl<64, kQT, PW, false, false>(ka, stream);
 }

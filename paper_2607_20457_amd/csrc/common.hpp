@@ -135,7 +135,7 @@ struct AttnLaunch {
   int64_t lse_zstride;
 };
 int launch_attention(const AttnLaunch& a, hipStream_t stream);
-int attn_rows_per_wg(int group);  // query rows covered by one attention workgroup
+int attn_rows_per_wg(int group, bool causal);  // query rows of one attention workgroup
 
 int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz, int Tq, int Hq,
                      int d, int64_t part_ostride, int64_t part_lstride, float* o, float* lse,

@@ -68,30 +68,51 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   const int32_t* seq = ids + b * L;
 
   for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = 0u;
+  // (the first round's barrier orders this against the atomics)
 
   // ---- pass 1: document frequency --------------------------------------
+  // The blocks are streamed as rounds of MAXIDF_THREADS x ROUND int4 groups;
+  // the loads of the next two rounds are in flight while a round's ids are
+  // marked, so each thread overlaps its atomics with HBM latency.
+  constexpr int ROUND = 2;
   const int nvec = Lb >> 2;  // int4 groups per block
-  for (int j = 0; j < num_blocks; ++j) {
-    for (int w = tid; w < vocab_w32; w += MAXIDF_THREADS) bits[w] = 0u;
-    __syncthreads();
-    const int4* blk = reinterpret_cast<const int4*>(seq + (int64_t)j * Lb);
-    for (int v0 = 0; v0 < nvec; v0 += 4 * MAXIDF_THREADS) {
-      int4 t4[4];
+  const int4* seq4 = reinterpret_cast<const int4*>(seq);
+  const int rpb = (nvec + MAXIDF_THREADS * ROUND - 1) / (MAXIDF_THREADS * ROUND);
+  const int rounds = num_blocks * rpb;
+  auto load_round = [&](int rd, int4 (&t)[ROUND]) {
+    const int j = rd / rpb;
+    const int r = rd - j * rpb;
+    const int4* blk = seq4 + (int64_t)j * nvec;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int v = v0 + u * MAXIDF_THREADS + tid;
-        t4[u] = v < nvec ? blk[v] : make_int4(-1, -1, -1, -1);
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        mark_token(t4[u].x, vocab, bits, dfw);
-        mark_token(t4[u].y, vocab, bits, dfw);
-        mark_token(t4[u].z, vocab, bits, dfw);
-        mark_token(t4[u].w, vocab, bits, dfw);
-      }
+    for (int u = 0; u < ROUND; ++u) {
+      const int v = (r * ROUND + u) * MAXIDF_THREADS + tid;
+      t[u] = v < nvec ? blk[v] : make_int4(-1, -1, -1, -1);
     }
-    __syncthreads();
+  };
+  int4 c0[ROUND], c1[ROUND], c2[ROUND];
+  if (rounds > 0) load_round(0, c0);
+  if (rounds > 1) load_round(1, c1);
+  for (int rd = 0; rd < rounds; ++rd) {
+    if (rd % rpb == 0) {  // a new block: everyone is done with the previous bitmap
+      __syncthreads();
+      for (int w = tid; w < vocab_w32; w += MAXIDF_THREADS) bits[w] = 0u;
+      __syncthreads();
+    }
+    if (rd + 2 < rounds) load_round(rd + 2, c2);
+#pragma unroll
+    for (int u = 0; u < ROUND; ++u) {
+      mark_token(c0[u].x, vocab, bits, dfw);
+      mark_token(c0[u].y, vocab, bits, dfw);
+      mark_token(c0[u].z, vocab, bits, dfw);
+      mark_token(c0[u].w, vocab, bits, dfw);
+    }
+#pragma unroll
+    for (int u = 0; u < ROUND; ++u) {
+      c0[u] = c1[u];
+      c1[u] = c2[u];
+    }
   }
+  __syncthreads();
 
   // ---- optional IDF table (Eq. idf) -------------------------------------
   if (idf) {
@@ -104,24 +125,46 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   }
 
   // ---- pass 2: per-chunk minimum df -------------------------------------
+  // Groups of PF int4 loads per thread, double-buffered: group g+1 is in
+  // flight while group g is reduced.  Every lane runs the same trip count,
+  // so all lanes join the cross-lane minimum.
+  constexpr int PF = 4;
   const int64_t nvec_seq = L >> 2;
   const int group = chunk >> 2;  // lanes per chunk (1..64)
   const int64_t nchunks_seq = L >> chunk_log2;
-  const int4* seq4 = reinterpret_cast<const int4*>(seq);
-  for (int64_t v0 = 0; v0 < nvec_seq; v0 += MAXIDF_THREADS) {
-    const int64_t v = v0 + tid;  // uniform trip count: every lane joins the shuffles
-    uint32_t mn = 255u;
-    if (v < nvec_seq) {
-      const int4 t4 = seq4[v];
-      mn = min(min(df_of(t4.x, vocab, df8), df_of(t4.y, vocab, df8)),
-               min(df_of(t4.z, vocab, df8), df_of(t4.w, vocab, df8)));
+  const int64_t n_iter = (nvec_seq + MAXIDF_THREADS - 1) / MAXIDF_THREADS;
+  const int64_t n_grp = (n_iter + PF - 1) / PF;
+  auto load_group = [&](int64_t gi, int4 (&t)[PF]) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int64_t v = (gi * PF + p) * MAXIDF_THREADS + tid;
+      t[p] = v < nvec_seq ? seq4[v] : make_int4(-1, -1, -1, -1);
     }
-    for (int off = 1; off < group; off <<= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off, 64));
-    if ((lane & (group - 1)) == 0 && v < nvec_seq) {
-      const int64_t c = v / group;
-      cmin[c] = (uint8_t)mn;
-      if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
+  };
+  auto reduce_group = [&](int64_t gi, const int4 (&t)[PF]) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int64_t it = gi * PF + p;
+      if (it >= n_iter) break;  // uniform across the workgroup
+      const int64_t v = it * MAXIDF_THREADS + tid;
+      uint32_t mn = min(min(df_of(t[p].x, vocab, df8), df_of(t[p].y, vocab, df8)),
+                        min(df_of(t[p].z, vocab, df8), df_of(t[p].w, vocab, df8)));
+      for (int off = 1; off < group; off <<= 1)
+        mn = min(mn, (uint32_t)__shfl_xor((int)mn, off, 64));
+      if ((lane & (group - 1)) == 0 && v < nvec_seq) {
+        const int64_t c = v / group;
+        cmin[c] = (uint8_t)mn;
+        if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
+      }
     }
+  };
+  int4 ga[PF], gb[PF];
+  if (n_grp > 0) load_group(0, ga);
+  for (int64_t gi = 0; gi < n_grp; gi += 2) {
+    if (gi + 1 < n_grp) load_group(gi + 1, gb);
+    reduce_group(gi, ga);
+    if (gi + 2 < n_grp) load_group(gi + 2, ga);
+    if (gi + 1 < n_grp) reduce_group(gi + 1, gb);
   }
   __syncthreads();
 
