@@ -71,8 +71,9 @@ int pulsar_version(void);
  * maximum IDF does because the logarithm is strictly decreasing.
  *
  * ids         int32 [batch, L], each in [0, vocab); 16-byte aligned.
- *             Ids outside that range are the caller's error: they are
- *             skipped (no memory fault) and the result is unspecified.
+ *             Ids outside that range are the caller's error: the kernel
+ *             never reads or writes outside its tables because of them, and
+ *             the result is unspecified.
  * sel_chunks  out int32 [batch, num_blocks, topk], chunk indices within the
  *             block, ascending.
  * chunk_mindf out int32 [batch, num_blocks, Lb / chunk], nullable: the

@@ -28,30 +28,73 @@
 
 static inline int64_t round_up4(int64_t x) { return (x + 3) & ~int64_t(3); }
 
+// Bitmap words: a power of two at least vocab/32 when that still fits next
+// to the df table (vocab up to 131072 here), so that the bitmap can be
+// scattered (see mark_token); otherwise exactly ceil(vocab/32), unscattered.
+static int64_t bitmap_words(int vocab) {
+  const int64_t need = ((int64_t)vocab + 31) / 32;
+  int64_t w = 1;
+  while (w < need) w <<= 1;
+  return round_up4(vocab) + w * 4 <= PULSAR_LDS_BYTES ? w : need;
+}
+
 // LDS layout: df bytes [round_up4(vocab)], then a region reused as the
 // per-block bitmap (pass 1) and the chunk minima (pass 2 / select).
 size_t maxidf_lds_bytes(int64_t L, int chunk, int vocab) {
   int64_t df_bytes = round_up4(vocab);
-  int64_t bitmap_bytes = ((int64_t)vocab + 31) / 32 * 4;
+  int64_t bitmap_bytes = bitmap_words(vocab) * 4;
   int64_t chunk_bytes = round_up4(L / chunk);
   return (size_t)(df_bytes + (bitmap_bytes > chunk_bytes ? bitmap_bytes : chunk_bytes));
 }
 
-__device__ __forceinline__ void mark_token(int t, int vocab, uint32_t* bits, uint32_t* dfw) {
-  if ((unsigned)t >= (unsigned)vocab) return;  // caller error: skipped, never out of bounds
-  const uint32_t bit = 1u << (t & 31);
-  const uint32_t old = atomicOr(&bits[t >> 5], bit);
-  if (!(old & bit)) atomicAdd(&dfw[t >> 2], 1u << ((t & 3) * 8));
+// Token t owns bit t%32 of bitmap word (t/32) XOR ((t%32)*129 mod W): a
+// bijection onto (word, bit) pairs that sends the 32 ids sharing a word --
+// under a Zipf law the most frequent ids, half of all tokens -- to 32
+// different words in 32 different banks, so their atomics do not serialise.
+// The n ids of one thread are marked with all bitmap atomics issued before
+// any result is used; the first setter of a bit adds one to the id's df
+// byte.  A negative id marks nothing (the loader pads partial rounds with -1);
+// an id at or above vocab is the caller's error, clamped into range so that
+// no access leaves the table, with an unspecified result.
+template <int n>
+__device__ __forceinline__ void mark_tokens(const int (&t)[n], int vocab, int spread_mask,
+                                            uint32_t* bits, uint32_t* dfw) {
+  uint32_t bit[n], old[n];
+  int word[n], ts[n];
+#pragma unroll
+  for (int i = 0; i < n; ++i) {
+    ts[i] = (int)min((uint32_t)t[i], (uint32_t)(vocab - 1));
+    const int b = ts[i] & 31;
+    word[i] = (ts[i] >> 5) ^ (((b << 7) | b) & spread_mask);
+    bit[i] = t[i] >= 0 ? 1u << b : 0u;  // -1 pads a partial round: marks nothing
+  }
+#pragma unroll
+  for (int i = 0; i < n; ++i) old[i] = atomicOr(&bits[word[i]], bit[i]);
+#pragma unroll
+  for (int i = 0; i < n; ++i)
+    if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] & 3) * 8));
 }
 
 __device__ __forceinline__ uint32_t df_of(int t, int vocab, const uint8_t* df8) {
-  return (unsigned)t < (unsigned)vocab ? (uint32_t)df8[t] : 255u;
+  return df8[min((uint32_t)t, (uint32_t)(vocab - 1))];
+}
+
+// Minimum over aligned groups of `group` lanes (a power of two); DPP within
+// rows of 16 lanes, cross-lane permutes beyond.
+__device__ __forceinline__ uint32_t group_min(uint32_t x, int group) {
+  if (group >= 2) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));
+  if (group >= 4) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));
+  if (group >= 8) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));
+  if (group >= 16) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));
+  if (group >= 32) x = min(x, (uint32_t)__shfl_xor((int)x, 16, 64));
+  if (group >= 64) x = min(x, (uint32_t)__shfl_xor((int)x, 32, 64));
+  return x;
 }
 
 __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
     const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2,
-    int topk, int vocab, int32_t* __restrict__ sel, int32_t* __restrict__ chunk_mindf,
-    float* __restrict__ idf) {
+    int topk, int vocab, int n_bitmap, int spread_mask, int32_t* __restrict__ sel,
+    int32_t* __restrict__ chunk_mindf, float* __restrict__ idf) {
   extern __shared__ uint32_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -59,7 +102,6 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   const int64_t b = blockIdx.x;
   const int chunk = 1 << chunk_log2;
   const int vocab_w4 = (vocab + 3) >> 2;
-  const int vocab_w32 = (vocab + 31) >> 5;
   uint32_t* dfw = lds;
   uint8_t* df8 = reinterpret_cast<uint8_t*>(lds);
   uint32_t* bits = lds + vocab_w4;
@@ -86,7 +128,8 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
 #pragma unroll
     for (int u = 0; u < ROUND; ++u) {
       const int v = (r * ROUND + u) * MAXIDF_THREADS + tid;
-      t[u] = v < nvec ? blk[v] : make_int4(-1, -1, -1, -1);
+      const int4 x = blk[min(v, nvec - 1)];
+      t[u] = v < nvec ? x : make_int4(-1, -1, -1, -1);
     }
   };
   int4 c0[ROUND], c1[ROUND], c2[ROUND];
@@ -95,16 +138,20 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   for (int rd = 0; rd < rounds; ++rd) {
     if (rd % rpb == 0) {  // a new block: everyone is done with the previous bitmap
       __syncthreads();
-      for (int w = tid; w < vocab_w32; w += MAXIDF_THREADS) bits[w] = 0u;
+      for (int w = tid; w < n_bitmap; w += MAXIDF_THREADS) bits[w] = 0u;
       __syncthreads();
     }
     if (rd + 2 < rounds) load_round(rd + 2, c2);
+    {
+      int tk[4 * ROUND];
 #pragma unroll
-    for (int u = 0; u < ROUND; ++u) {
-      mark_token(c0[u].x, vocab, bits, dfw);
-      mark_token(c0[u].y, vocab, bits, dfw);
-      mark_token(c0[u].z, vocab, bits, dfw);
-      mark_token(c0[u].w, vocab, bits, dfw);
+      for (int u = 0; u < ROUND; ++u) {
+        tk[4 * u] = c0[u].x;
+        tk[4 * u + 1] = c0[u].y;
+        tk[4 * u + 2] = c0[u].z;
+        tk[4 * u + 3] = c0[u].w;
+      }
+      mark_tokens(tk, vocab, spread_mask, bits, dfw);
     }
 #pragma unroll
     for (int u = 0; u < ROUND; ++u) {
@@ -129,30 +176,30 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   // flight while group g is reduced.  Every lane runs the same trip count,
   // so all lanes join the cross-lane minimum.
   constexpr int PF = 4;
-  const int64_t nvec_seq = L >> 2;
-  const int group = chunk >> 2;  // lanes per chunk (1..64)
-  const int64_t nchunks_seq = L >> chunk_log2;
-  const int64_t n_iter = (nvec_seq + MAXIDF_THREADS - 1) / MAXIDF_THREADS;
-  const int64_t n_grp = (n_iter + PF - 1) / PF;
-  auto load_group = [&](int64_t gi, int4 (&t)[PF]) {
+  const int nvec_seq = (int)(L >> 2);  // L < 2^31 (checked by the caller)
+  const int group = chunk >> 2;        // lanes per chunk (1..64)
+  const int group_log2 = chunk_log2 - 2;
+  const int nchunks_seq = (int)(L >> chunk_log2);
+  const int n_iter = (nvec_seq + MAXIDF_THREADS - 1) / MAXIDF_THREADS;
+  const int n_grp = (n_iter + PF - 1) / PF;
+  auto load_group = [&](int gi, int4 (&t)[PF]) {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      const int64_t v = (gi * PF + p) * MAXIDF_THREADS + tid;
-      t[p] = v < nvec_seq ? seq4[v] : make_int4(-1, -1, -1, -1);
+      const int v = (gi * PF + p) * MAXIDF_THREADS + tid;
+      t[p] = seq4[min(v, nvec_seq - 1)];
     }
   };
-  auto reduce_group = [&](int64_t gi, const int4 (&t)[PF]) {
+  auto reduce_group = [&](int gi, const int4 (&t)[PF]) {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      const int64_t it = gi * PF + p;
+      const int it = gi * PF + p;
       if (it >= n_iter) break;  // uniform across the workgroup
-      const int64_t v = it * MAXIDF_THREADS + tid;
+      const int v = it * MAXIDF_THREADS + tid;
       uint32_t mn = min(min(df_of(t[p].x, vocab, df8), df_of(t[p].y, vocab, df8)),
                         min(df_of(t[p].z, vocab, df8), df_of(t[p].w, vocab, df8)));
-      for (int off = 1; off < group; off <<= 1)
-        mn = min(mn, (uint32_t)__shfl_xor((int)mn, off, 64));
+      mn = group_min(mn, group);
       if ((lane & (group - 1)) == 0 && v < nvec_seq) {
-        const int64_t c = v / group;
+        const int c = v >> group_log2;
         cmin[c] = (uint8_t)mn;
         if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
       }
@@ -160,7 +207,7 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   };
   int4 ga[PF], gb[PF];
   if (n_grp > 0) load_group(0, ga);
-  for (int64_t gi = 0; gi < n_grp; gi += 2) {
+  for (int gi = 0; gi < n_grp; gi += 2) {
     if (gi + 1 < n_grp) load_group(gi + 1, gb);
     reduce_group(gi, ga);
     if (gi + 2 < n_grp) load_group(gi + 2, ga);
@@ -228,8 +275,10 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
   if (hipFuncSetAttribute((const void*)maxidf_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds_bytes) != hipSuccess)
     return PULSAR_EHIP;
+  const int64_t nb = bitmap_words(vocab);
+  const bool pow2 = (nb & (nb - 1)) == 0;
   hipLaunchKernelGGL(maxidf_kernel, dim3(batch), dim3(MAXIDF_THREADS), lds_bytes, stream, ids, L,
-                     num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, sel, chunk_mindf,
-                     idf);
+                     num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, (int)nb,
+                     pow2 ? (int)(nb - 1) : 0, sel, chunk_mindf, idf);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
