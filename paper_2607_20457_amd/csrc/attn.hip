@@ -155,8 +155,14 @@ void attn_fwd_kernel(KernelArgs ka) {
 #pragma unroll
     for (int s = 0; s < DS; ++s) qf[t][s] = r < a.n_q ? src[2 * s] : bf16x8{};
   }
-  // Drain the Q loads here, so that no wait inside the key loop is tied to them.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // Wait for the Q loads here: passing each fragment through an empty asm
+  // statement makes the compiler wait for it before the loop and treat it as
+  // defined afterwards, so no wait inside the key loop is tied to the Q loads
+  // (which would also wait for the next tile's prefetch issued after them).
+#pragma unroll
+  for (int t = 0; t < QT; ++t)
+#pragma unroll
+    for (int s = 0; s < DS; ++s) asm volatile("" : "+v"(qf[t][s]));
 
   f32x16 acc[DT][QT];
   float m_ref[QT], l_run[QT], lr_run[QT];  // reference max, fp32 weight sum, bf16 weight sum
