@@ -22,18 +22,22 @@
 //                 reference (the row's maximum over the first 32 keys), so the
 //                 O accumulator is only ever touched by the matrix cores; the
 //                 final division by the weight sum makes the result exact.
-//                 Should a weight exceed 2^64 (a later score far above the
-//                 reference), the workgroup repeats the pass with the classic
-//                 online softmax, which raises the running maximum and
-//                 rescales O.  P enters the PV product rounded to bf16; O is
+//                 Should the weight sum exceed 2^88 (a later score far above
+//                 the reference), the workgroup repeats the pass with the
+//                 classic online softmax, which raises the running maximum
+//                 and rescales O.  P enters the PV product rounded to bf16; O is
 //                 divided by the sum of those rounded weights (an exact convex
 //                 combination), while the LSE uses the fp32 sum.
-//   O^T += V^T P^T  A = V^T from LDS (V is transposed on its way into LDS),
-//                 B = P, which is already in the B-operand layout because K
-//                 rows are stored in LDS with bits 2 and 3 of the key index
-//                 swapped.
-//   K/V tiles are double-buffered: the next tile's global loads are issued
-//   before the current tile's math and written to LDS after it.
+//   O^T += V^T P^T  A = V^T from LDS; B = P, which is already in the
+//                 B-operand layout because K rows are stored in LDS with bits
+//                 2 and 3 of the key index swapped.
+//   K tiles move from HBM to LDS by buffer loads that write LDS directly;
+//   V tiles pass through registers and are written transposed.  Three LDS
+//   stages; the K row padding (2d+16 B) keeps the K reads free of bank
+//   conflicts.
+//   The two wavefronts of a SIMD run ping-pong: one multiplies (PV of the
+//   previous tile, S of the current one) while the other computes weights,
+//   with a workgroup barrier between phases.
 #include <type_traits>
 
 #include "common.hpp"
@@ -46,16 +50,20 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer access (word 3 of the resource)
 __device__ constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+
 template <int D>
 struct Tile {
-  static constexpr int K_STRIDE = D * 2 + 16;   // bytes per K row in LDS (padded)
-  static constexpr int V_STRIDE = BN * 2 + 16;  // bytes per V^T row (one head_dim entry)
-  static constexpr int K_BYTES = BN * K_STRIDE;
+  static constexpr int CPR = D / 8;               // 16-byte data chunks per row
+  static constexpr int K_CH = CPR + 1;            // K row: data + one pad chunk
+  static constexpr int K_STRIDE = 16 * K_CH;      // bytes per K row in LDS
+  static constexpr int V_STRIDE = BN * 2 + 16;    // bytes per V^T row (one head_dim entry)
+  static constexpr int K_BYTES = BN * K_STRIDE;   // = K_CH KiB
   static constexpr int V_BYTES = D * V_STRIDE;
   static constexpr int STAGE = K_BYTES + V_BYTES;
-  static constexpr int LDS = 2 * STAGE + 2 * BN * 4;  // two stages + two position rows
-  static constexpr int CPR = D / 8;               // 16-byte chunks per row
-  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= threads)
+  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= 256)
+  static constexpr int LDS = 3 * STAGE + 3 * BN * 4;  // three stages + three position rows
 };
 
 struct KernelArgs {
@@ -68,16 +76,25 @@ struct KernelArgs {
   int nz;             // z extent (sequences, or shards x splits)
 };
 
+// One 16-byte-per-lane buffer load that writes LDS directly: lane l's 16
+// bytes land at LDS byte lds_base + 16*l.  Issued from asm so that the
+// compiler does not order the key loop's LDS reads after it (it cannot tell
+// that they read the other stage); the loop waits for it explicitly
+// (vmcnt) before the barrier that publishes the stage.
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t rsrc, uint32_t voffset,
+                                          uint32_t lds_base) {
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(voffset), "s"(rsrc), "{m0}"(lds_base)
+               : "memory");
+}
+
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r >> 1) & 4) | ((r << 1) & 8);
 }
 
-__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) {
-  return (a & 0xFFFFu) | (b << 16);
-}
-__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) {
-  return (a >> 16) | (b & 0xFFFF0000u);
-}
+// Matrix-phase fragment reads run this many matrix steps ahead.
+constexpr int MDEPTH = 4;
 
 template <int D, int QT, int WAVES, bool CAUSAL, bool LSE>
 __global__ __launch_bounds__(64 * WAVES) __attribute__((amdgpu_waves_per_eu(3 - QT, 3 - QT)))
@@ -87,13 +104,13 @@ void attn_fwd_kernel(KernelArgs ka) {
   constexpr int QR = 32 * QT;        // rows per wavefront
   constexpr int DS = D / 16;         // k-steps of the S product
   constexpr int DT = D / 32;         // 32-row tiles of O^T
-  constexpr int KR = BN * T::CPR / THREADS;  // consecutive K rows loaded per thread
+  constexpr int SEG_PER_WAVE = (T::K_CH + 3) / 4;  // K segments per group-1 wave
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const AttnLaunch& a = ka.a;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31;
   const int g = lane >> 5;
 
@@ -127,15 +144,14 @@ void attn_fwd_kernel(KernelArgs ka) {
   const uint16_t* Vz = a.V + zkv * a.kv_zstride + (int64_t)kvh * D;
   const float c2 = a.scale_log2;
 
-  uint8_t* stage0 = smem;
-  int32_t* lpos = reinterpret_cast<int32_t*>(smem + 2 * T::STAGE);  // [2][BN]
-  int* run_base = lpos + 2 * BN;                                      // [map.n_runs]
+  lds_u8* const stage0 = (lds_u8*)smem;  // LDS address space: reads take immediate offsets
+  int32_t* lpos = reinterpret_cast<int32_t*>(smem + 3 * T::STAGE);  // [3][BN]
+  int* run_base = lpos + 3 * BN;                                      // [map.n_runs]
   build_run_table(a.map, sel, run_base, tid, THREADS);
   __syncthreads();
 
   // K/V rows are read through buffer resources covering this sequence (or
-  // shard); a padded key has position -1, whose offset falls outside the
-  // resource, so the hardware returns zeros for it.
+  // shard), with 32-bit byte offsets.
   const uint32_t row_bytes = (uint32_t)(a.Hkv * D * 2);
   const __amdgpu_buffer_rsrc_t k_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(a.K + zkv * a.kv_zstride), (short)0, (int)(a.kv_zstride * 2),
@@ -167,81 +183,91 @@ void attn_fwd_kernel(KernelArgs ka) {
   f32x16 acc[DT][QT];
   float m_ref[QT], l_run[QT], lr_run[QT];  // reference max, fp32 weight sum, bf16 weight sum
 
-  // ---- cooperative tile loads -----------------------------------------------
-  // K: thread t loads rows KR*(t/CPR) .. +KR-1 at 16-byte chunk t%CPR.
-  // V: thread t (t < 16*CPR) loads rows 4*(t%16) .. +3 at chunk t/16 and
-  //    writes them transposed (head_dim-major) into LDS.
+  // ---- tile loads --------------------------------------------------------------
+  // Wave 0 writes the global positions of a tile's 64 keys to LDS (-1 past
+  // the end).
+  // K: the four group-1 waves move the K tile straight into LDS, in K_CH
+  //   segments of 1 KiB (pad chunks included); wave 4+w issues segments w,
+  //   w+4, ...  Lane l of segment sg fills the 16 bytes at byte 16*l of it:
+  //   slot 64*sg + l, i.e. row slot / K_CH, chunk slot % K_CH.  K row r holds
+  //   key swap_bits23(r).  A pad chunk re-reads chunk 0 of its row, and a key
+  //   past the end reads row 0 of the sequence: both finite, never weighted.
+  // V: group-0 thread t (t < V_UNITS) loads keys 4*(t%16) .. +3 at 16-byte
+  //   chunk t/16 into registers and writes them transposed (head_dim-major)
+  //   into LDS, so that the PV product reads V^T fragments with 16-byte
+  //   reads.  A key past the end has position -1, whose offset falls outside
+  //   the buffer resource, so the hardware returns zeros for it.
   auto tile_positions = [&](int j, int32_t* dst) {
     if (tid < BN) {
       const int k = kv_begin + j * BN + tid;
       dst[tid] = k < kv_end ? row_position(a.map, run_base, k) : -1;
     }
   };
-  u32x4 kreg[KR];
-  u32x4 vreg[4];
-  const bool v_thread = tid < T::V_UNITS;
-  auto load_regs = [&](const int32_t* pos) {
-    const int kr0 = KR * (tid / T::CPR);
-    int kp[KR];
-    if constexpr (KR == 4) {
-      const int4 p4 = *reinterpret_cast<const int4*>(pos + kr0);
-      kp[0] = p4.x; kp[1] = p4.y; kp[2] = p4.z; kp[3] = p4.w;
-    } else {
+  int dma_row[SEG_PER_WAVE];
+  uint32_t dma_col[SEG_PER_WAVE];
+  const int wk = wave - 4;  // group-1 wave index
 #pragma unroll
-      for (int i = 0; i < KR; ++i) kp[i] = pos[kr0 + i];
-    }
-    const uint32_t kcol = head_off + (uint32_t)(tid % T::CPR) * 16;
+  for (int i = 0; i < SEG_PER_WAVE; ++i) {
+    const int slot = (wk + 4 * i) * 64 + lane;
+    const int r = slot / T::K_CH;
+    const int col = slot - r * T::K_CH;
+    dma_row[i] = swap_bits23(r & (BN - 1));
+    dma_col[i] = head_off + (uint32_t)(col < T::CPR ? col : 0) * 16;
+  }
+  auto issue_k = [&](const int32_t* pos, lds_u8* st) {
+    const uint32_t st_lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)st);
+    int p[SEG_PER_WAVE];  // all positions first: each asm load orders later LDS reads
 #pragma unroll
-    for (int i = 0; i < KR; ++i)
-      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(k_rsrc, (int)((uint32_t)kp[i] * row_bytes + kcol),
-                                                      0, 0);
-    if (v_thread) {
-      const int4 p4 = *reinterpret_cast<const int4*>(pos + 4 * (tid & 15));
-      const int vp[4] = {p4.x, p4.y, p4.z, p4.w};
-      const uint32_t vcol = head_off + (uint32_t)(tid >> 4) * 16;
+    for (int i = 0; i < SEG_PER_WAVE; ++i) p[i] = wk + 4 * i < T::K_CH ? pos[dma_row[i]] : 0;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        vreg[rr] = __builtin_amdgcn_raw_buffer_load_b128(
-            v_rsrc, (int)((uint32_t)vp[rr] * row_bytes + vcol), 0, 0);
+    for (int i = 0; i < SEG_PER_WAVE; ++i) {
+      const int sg = wk + 4 * i;
+      if (sg < T::K_CH)
+        lds_dma16(k_rsrc, (uint32_t)max(p[i], 0) * row_bytes + dma_col[i], st_lds + sg * 1024);
     }
   };
-  auto store_lds = [&](uint8_t* st) {
-    const int kr0 = KR * (tid / T::CPR);
+  // group 0 only (V_UNITS <= 256, a multiple of 64: uniform per wave)
+  const bool v_thread = wave * 64 < T::V_UNITS;
+  u32x4 vreg[4];
+  auto load_v = [&](const int32_t* pos) {
+    const int4 p4 = *reinterpret_cast<const int4*>(pos + 4 * (tid & 15));
+    const int vp[4] = {p4.x, p4.y, p4.z, p4.w};
+    const uint32_t vcol = head_off + (uint32_t)(tid >> 4) * 16;
 #pragma unroll
-    for (int i = 0; i < KR; ++i)
-      *reinterpret_cast<u32x4*>(st + swap_bits23(kr0 + i) * T::K_STRIDE + (tid % T::CPR) * 16) =
-          kreg[i];
-    if (v_thread) {
-      uint8_t* sv = st + T::K_BYTES;
-      const int kq = tid & 15;
-      const int dc = tid >> 4;
+    for (int rr = 0; rr < 4; ++rr)
+      vreg[rr] = __builtin_amdgcn_raw_buffer_load_b128(v_rsrc, (int)((uint32_t)vp[rr] * row_bytes + vcol),
+                                                       0, 0);
+  };
+  auto store_v = [&](lds_u8* st) {
+    lds_u8* sv = st + T::K_BYTES;
+    const int kq = tid & 15;
+    const int dc = tid >> 4;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
-        const u32x2 lo = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x05040100u),
-                          __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x05040100u)};
-        const u32x2 hi = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x07060302u),
-                          __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x07060302u)};
-        *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
-        *reinterpret_cast<u32x2*>(sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
-      }
+    for (int w = 0; w < 4; ++w) {
+      // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
+      const u32x2 lo = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x05040100u),
+                        __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x05040100u)};
+      const u32x2 hi = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x07060302u),
+                        __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x07060302u)};
+      *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(
+          sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
+      *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(
+          sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
     }
   };
 
   // ---- building blocks of one 32-key half --------------------------------------
   // S^T of keys u*32..u*32+31 of the tile in LDS against this wave's queries.
-  auto s_product = [&](const uint8_t* sK, int u, f32x16 (&S)[QT]) {
-#pragma unroll
-    for (int t = 0; t < QT; ++t) S[t] = f32x16{};
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
-                                                         (16 * s + 8 * g) * 2);
-#pragma unroll
-      for (int t = 0; t < QT; ++t)
-        S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][s], S[t], 0, 0, 0);
-    }
+  auto k_frag = [&](const lds_u8* sK, int u, int s) {
+    return *reinterpret_cast<const lds_bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
+                                                (16 * s + 8 * g) * 2);
   };
+  auto v_frag = [&](const lds_u8* sV, int u, int c, int e) {
+    return *reinterpret_cast<const lds_bf16x8*>(sV + (e * 32 + l32) * T::V_STRIDE +
+                                                (u * 32 + 16 * c + 8 * g) * 2);
+  };
+
+
   // -inf for keys after the query row (causal) or past the last key.
   auto apply_mask = [&](int kh, f32x16 (&S)[QT]) {
 #pragma unroll
@@ -286,18 +312,7 @@ void attn_fwd_kernel(KernelArgs ka) {
       if (LSE) l_run[t] += psum;
     }
   };
-  auto pv_product = [&](const uint8_t* sV, int u, const bf16x8 (&pf)[2][QT]) {
-#pragma unroll
-    for (int e = 0; e < DT; ++e)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-            sV + (e * 32 + l32) * T::V_STRIDE + (u * 32 + 16 * c + 8 * g) * 2);
-#pragma unroll
-        for (int t = 0; t < QT; ++t)
-          acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[c][t], acc[e][t], 0, 0, 0);
-      }
-  };
+
 
   auto reset = [&]() {
 #pragma unroll
@@ -311,79 +326,145 @@ void attn_fwd_kernel(KernelArgs ka) {
       lr_run[t] = 0.f;
     }
   };
-  // Tile 0 written to stage 0 and tile 1's positions staged.
-  auto prologue = [&]() {
-    tile_positions(0, lpos);
-    __syncthreads();
-    if (ntiles > 1) tile_positions(1, lpos + BN);
-    load_regs(lpos);
-    store_lds(stage0);
+  // ---- ping-pong schedule ------------------------------------------------
+  // Waves 0-3 (group 0) and 4-7 (group 1) share the four SIMDs pairwise.
+  // Every wave alternates a matrix phase M_m (PV of tile m-1, then S of
+  // tile m) and a vector phase V_m (the weights of tile m), with a workgroup
+  // barrier after each phase; group 1 runs one phase behind group 0, so on
+  // every SIMD one wave's exponentials overlap the other wave's matrix
+  // instructions.  Between barriers k-1 and k, group 0 runs its phase k and
+  // group 1 its phase k-1 (phase 2m = M_m, 2m+1 = V_m).
+  //
+  // A half past every row of the wave (causal) or past the last key is
+  // still multiplied; the mask gives it zero weight.
+  //
+  // Tiles rotate through three LDS stages (tile t in stage t % 3).  Tile t's
+  // K is read in phases 2t and 2t+1 of the workgroup (S by group 0, then by
+  // group 1) and its V^T in phases 2t+2 and 2t+3 (PV).  Group 1 moves K_t
+  // into LDS during its V_{t-2} and waits for it at the end of its M_{t-1};
+  // group 0 loads V_t into registers during V_{t-1} and writes V^T_t during
+  // V_t.  Stage t % 3 last held tile t-3, whose last reader ran before
+  // either write.  Wave 0 writes tile t's key positions during V_{t-2}.
+  static_assert(WAVES == 8, "the ping-pong schedule pairs waves w and w+4 on one SIMD");
+  const int grp = wave >> 2;
+  // The stage offset goes through readfirstlane so that loop strength
+  // reduction keeps it one scalar (fragment reads then take immediate
+  // offsets from one base) instead of one induction variable per read.
+  auto stage_of = [&](int t) {
+    return stage0 + __builtin_amdgcn_readfirstlane((t % 3) * T::STAGE);
   };
-  // Iteration j: wait for tile j in LDS, prefetch tile j+1 into registers, run
-  // `body`, then store tile j+1 into the other buffer.
-  auto tile_loop = [&](auto&& body) {
-    for (int j = 0; j < ntiles; ++j) {
-      __syncthreads();
-      const int buf = j & 1;
-      if (j + 1 < ntiles) load_regs(lpos + (buf ^ 1) * BN);
-      if (j + 2 < ntiles) tile_positions(j + 2, lpos + buf * BN);
-      const uint8_t* sK = stage0 + buf * T::STAGE;
-      body(kv_begin + j * BN, sK, sK + T::K_BYTES);
-      if (j + 1 < ntiles) store_lds(stage0 + (buf ^ 1) * T::STAGE);
+  auto pos_of = [&](int t) { return lpos + (t % 3) * BN; };
+  auto key_of = [&](int t, int u) { return kv_begin + t * BN + 32 * u; };
+  auto edge = [&](int t, int u) {
+    const int kh = key_of(t, u);
+    return CAUSAL ? (kh + 31 > row0) : (kh + 32 > kv_end);
+  };
+  f32x16 S[2][QT];
+  bf16x8 P[2][2][QT];
+  // Matrix phase with every half live, as one block: PV of the previous
+  // tile (four independent accumulators), then S of this tile (two chains).
+  // Fragment reads run MDEPTH matrix steps ahead through a register ring,
+  // and a scheduling fence after each step keeps that order.
+  auto m_phase_full = [&](const lds_u8* sV, const lds_u8* sK) {
+    constexpr int NPV = 4 * DT, N = NPV + 2 * DS;
+    auto frag = [&](int i) -> bf16x8 {
+      if (i < NPV) return v_frag(sV, i / (2 * DT), (i / DT) % 2, i % DT);
+      return k_frag(sK, (i - NPV) % 2, (i - NPV) / 2);
+    };
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) S[u][t] = f32x16{};
+    bf16x8 ring[MDEPTH];
+#pragma unroll
+    for (int i = 0; i < MDEPTH; ++i) ring[i] = frag(i);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const bf16x8 f = ring[i % MDEPTH];
+      if (i + MDEPTH < N) ring[i % MDEPTH] = frag(i + MDEPTH);
+      if (i < NPV) {
+        const int u = i / (2 * DT), c = (i / DT) % 2, e = i % DT;
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          acc[e][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, P[u][c][t], acc[e][t], 0, 0, 0);
+      } else {
+        const int u = (i - NPV) % 2, sk = (i - NPV) / 2;
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          S[u][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[t][sk], S[u][t], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // ---- fast pass: fixed per-row reference, O touched only by MFMA -----------
-  // The reference is the row's maximum over the first 32 keys; only halves
-  // that reach past a query row (or past the last key) are masked.
-  bool overflow = false;
-  reset();
-  if (ntiles > 0) {
-    prologue();
-    __syncthreads();
-    f32x16 S[QT];
-    s_product(stage0, 0, S);
-    apply_mask(kv_begin, S);
-#pragma unroll
-    for (int t = 0; t < QT; ++t) m_ref[t] = row_max(S[t]);
-  }
-  tile_loop([&](int kbase, const uint8_t* sK, const uint8_t* sV) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int kh = kbase + 32 * u;
-      if (CAUSAL && kh > row0 + QR - 1) continue;  // every key after every row
-      f32x16 S[QT];
-      bf16x8 pf[2][QT];
-      s_product(sK, u, S);
-      if (CAUSAL ? (kh + 31 > row0) : (kh + 32 > kv_end)) apply_mask(kh, S);
-      weights(S, pf);
-      pv_product(sV, u, pf);
-    }
-  });
-  // Every weight is at most the final sum, so a finite sum below 2^88 bounds
-  // them all; above that (or not finite) the exact pass takes over.
-#pragma unroll
-  for (int t = 0; t < QT; ++t) overflow |= !(lr_run[t] <= 0x1p88f);
-
-  // ---- exact pass: classic online softmax, only after an overflow flag --------
-  // The running maximum is raised when a half's maximum exceeds it by more
-  // than 2^8, and O and the sums are rescaled.
-  if (__syncthreads_or(overflow)) {
-    __syncthreads();
+  // EXACT = false: fixed per-row reference (the row's maximum over the
+  // first 32 keys), O touched only by MFMA.  EXACT = true: classic online
+  // softmax; the running maximum is raised when a tile's maximum exceeds it
+  // by more than 2^8, and O and the sums are rescaled.
+  auto run_pass = [&](auto exact_tag) {
+    constexpr bool EXACT = decltype(exact_tag)::value;
     reset();
-    if (ntiles > 0) prologue();
-    tile_loop([&](int kbase, const uint8_t* sK, const uint8_t* sV) {
+    tile_positions(0, pos_of(0));
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int kh = kbase + 32 * u;
-        if (CAUSAL && kh > row0 + QR - 1) continue;
-        f32x16 S[QT];
-        bf16x8 pf[2][QT];
-        s_product(sK, u, S);
-        apply_mask(kh, S);
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int t = 0; t < QT; ++t) P[u][c][t] = bf16x8{};
+    for (int i = tid; i < T::V_BYTES / 16; i += THREADS)
+      reinterpret_cast<__attribute__((address_space(3))) u32x4*>(stage_of(2) + T::K_BYTES)[i] =
+          u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+    if (ntiles > 0) {
+      if (grp == 1) issue_k(pos_of(0), stage_of(0));
+      if (v_thread) load_v(pos_of(0));
+    }
+    if (ntiles > 1) tile_positions(1, pos_of(1));
+    if (grp == 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (grp == 1) {  // K of tile 1, then group 1's lag barrier
+      if (ntiles > 1) issue_k(pos_of(1), stage_of(1));
+      __syncthreads();
+    }
+    // The matrix phase runs at raised wave priority, so that the SIMD's
+    // arbiter issues its matrix instructions ahead of the partner wave's
+    // vector instructions whenever both are ready.
+    // Each phase ends in phase_barrier(): the scheduling fences keep
+    // arithmetic from moving across the workgroup barrier (it only orders
+    // memory), so that no phase's work leaks into the next interval.
+    auto phase_barrier = [&]() {
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto m_phase_begin = [&]() {
+      __builtin_amdgcn_s_setprio(1);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    auto m_phase_end = [&]() {
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
+      if (grp == 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      phase_barrier();
+    };
+    // V_m: weights of tile m (both halves; a half with no visible key is
+    // fully masked and weighs zero).
+    auto v_phase = [&](int m) {
+      if (grp == 1 && m + 2 < ntiles) issue_k(pos_of(m + 2), stage_of(m + 2));
+      if (v_thread) {  // V^T of tile m into its stage, then V of tile m+1 into registers
+        store_v(stage_of(m));
+        if (m + 1 < ntiles) load_v(pos_of(m + 1));
+      }
+      if (m + 2 < ntiles) tile_positions(m + 2, pos_of(m + 2));  // wave 0
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        if (EXACT || edge(m, u)) apply_mask(key_of(m, u), S[u]);
+      if (EXACT) {
+        // One raise per tile: both halves' weights enter O only in M_{m+1},
+        // so they must share the reference.
 #pragma unroll
         for (int t = 0; t < QT; ++t) {
-          const float mx = row_max(S[t]);
+          const float mx = fmaxf(row_max(S[0][t]), row_max(S[1][t]));
           const bool raise = mx > m_ref[t] + MAX_SLACK;
           const float m_use = raise ? mx : m_ref[t];
           if (__any(raise)) {
@@ -395,11 +476,34 @@ void attn_fwd_kernel(KernelArgs ka) {
           }
           m_ref[t] = m_use;
         }
-        weights(S, pf);
-        pv_product(sV, u, pf);
+      } else if (m == 0) {  // half 0 of tile 0 always has a visible key
+#pragma unroll
+        for (int t = 0; t < QT; ++t) m_ref[t] = row_max(S[0][t]);
       }
-    });
-  }
+      weights(S[0], P[0]);
+      weights(S[1], P[1]);
+      phase_barrier();
+    };
+    // Every matrix phase is the full one: M_0 multiplies the zeroed V^T of
+    // stage 2 by P = 0, and M_ntiles computes an S that is never used (from
+    // finite LDS data).
+    for (int m = 0; m <= ntiles; ++m) {
+      m_phase_begin();
+      m_phase_full(stage_of(m + 2) + T::K_BYTES, stage_of(m));
+      m_phase_end();
+      if (m < ntiles) v_phase(m);
+    }
+    if (grp == 0) __syncthreads();  // matches group 1's lag barrier
+  };
+
+  // ---- fast pass, then the exact pass only after an overflow flag -----------
+  run_pass(std::false_type{});
+  // Every weight is at most the final sum, so a finite sum below 2^88 bounds
+  // them all; above that (or not finite) the exact pass takes over.
+  bool overflow = false;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) overflow |= !(lr_run[t] <= 0x1p88f);
+  if (__syncthreads_or(overflow)) run_pass(std::true_type{});
 
   // ---- epilogue: normalise, write O and LSE ---------------------------------
 #pragma unroll
