@@ -105,7 +105,7 @@ __device__ __forceinline__ int wave_excl_scan(int x) {
 int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
                   int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
                   hipStream_t stream);
-size_t maxidf_lds_bytes(int64_t L, int chunk, int vocab);
+size_t maxidf_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab);
 
 int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
                      int n_rows, int32_t* pos, hipStream_t stream);

@@ -89,6 +89,15 @@ def test_max_blocks_and_large_vocab():
     _check(ids, 255, 16, 1, 140000, idf_too=False)
 
 
+@pytest.mark.parametrize("vocab", [32000, 128256])
+def test_chunk4_at_128k_layouts(vocab):
+    # 32768 chunk minima: with vocab 32000 they follow the df table in the
+    # compact layout; with vocab 128256 they no longer fit there and the
+    # general layout is used.
+    ids = workload.zipf_ids(77 + vocab, 131072, vocab)[None]
+    _check(ids, 16, 4, 9, vocab, idf_too=False)
+
+
 def test_deterministic():
     ids = to_dev_i32(workload.make_ids(workload.CONFIGS["llama8b_32k"], batch=2))
     a = P.maxidf_summaries(ids, 8, 32, 16, 128256, return_mindf=True)
