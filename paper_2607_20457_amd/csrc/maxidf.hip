@@ -21,7 +21,8 @@
 //     bytes behind it; pass 2 streams the ids again;
 //   * resident (compact, L <= 131072, blocks of a multiple of 8192 ids): pass
 //     1 keeps every thread's 128 ids in registers, packed, and pass 2 reads
-//     them back from there, so the ids cross HBM once.
+//     them back from there, so the ids cross HBM once; two bitmaps alternate
+//     between blocks, one barrier per block.
 //
 // A chunk's Max-IDF score ln(N / mindf) is strictly decreasing in mindf, so
 // ranking by (mindf ascending, index ascending) is ranking by (score
@@ -56,6 +57,9 @@ constexpr int kFastVocab = kFastWords * 32;
 // of 4 ids per thread, at most RES_ROUNDS of them per sequence.
 constexpr int RES_ROUNDS = 16;
 constexpr int RES_ROUND_TOKENS = MAXIDF_THREADS * 8;
+// The resident variant alternates two compact bitmaps (block j marks bitmap
+// j % 2 and clears the other), so its df bytes start at byte 32768.
+constexpr int kResBitmapBytes = 2 * kFastBitmapBytes;
 
 struct MaxidfPlan {
   bool fast;
@@ -70,12 +74,13 @@ static MaxidfPlan maxidf_plan(int64_t L, int num_blocks, int chunk, int vocab) {
   const int64_t df_bytes = round_up4(vocab);
   const int64_t chunk_bytes = round_up4(L / chunk);
   if (vocab <= kFastVocab) {
+    if (L <= (int64_t)RES_ROUNDS * RES_ROUND_TOKENS && (L / num_blocks) % RES_ROUND_TOKENS == 0 &&
+        chunk_bytes <= kResBitmapBytes)  // static LDS: bitmaps + the largest df table
+      return {true, true, kResBitmapBytes + kFastVocab, 0};
     const bool in_bitmap = chunk_bytes <= kFastBitmapBytes;
     const int64_t lds = kFastBitmapBytes + df_bytes + (in_bitmap ? 0 : chunk_bytes);
-    const bool resident = L <= (int64_t)RES_ROUNDS * RES_ROUND_TOKENS &&
-                          (L / num_blocks) % RES_ROUND_TOKENS == 0;
     if (lds <= PULSAR_LDS_BYTES)
-      return {true, resident, lds, in_bitmap ? 0 : kFastBitmapBytes + df_bytes};
+      return {true, false, lds, in_bitmap ? 0 : kFastBitmapBytes + df_bytes};
   }
   const int64_t bitmap_bytes = bitmap_words(vocab) * 4;
   return {false, false, df_bytes + (bitmap_bytes > chunk_bytes ? bitmap_bytes : chunk_bytes),
@@ -111,7 +116,7 @@ __device__ __forceinline__ void mark_tokens(const int (&t)[n], int vocab, int sp
   for (int i = 0; i < n; ++i) old[i] = atomicOr(&bits[word[i]], bit[i]);
 #pragma unroll
   for (int i = 0; i < n; ++i)
-    if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] & 3) * 8));
+    if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] << 3) & 31));
 }
 
 // Compact layout: the first setter of a token's bit in this block adds one
@@ -132,7 +137,7 @@ __device__ __forceinline__ void mark_tokens_compact(const int (&t)[n], uint32_t 
   for (int i = 0; i < n; ++i) old[i] = atomicOr(&bits[ts[i] & (kFastWords - 1)], bit[i]);
 #pragma unroll
   for (int i = 0; i < n; ++i)
-    if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] & 3) * 8));
+    if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] << 3) & 31));
 }
 
 __device__ __forceinline__ uint32_t df_of(int t, int vocab, const uint8_t* df8) {
@@ -161,59 +166,47 @@ __device__ void write_idf(const uint8_t* df8, int vocab, int num_blocks, float* 
   }
 }
 
+// Lanes below this one with their bit set in a wave mask.
+__device__ __forceinline__ int count_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
 // Top-k chunks of every block of sequence b from the chunk minima cmin
 // ([num_blocks][C] bytes in LDS), written in ascending chunk order.  One
-// wavefront per block: the threshold tau is the smallest df with at least k
-// chunks at or below it (binary search over 1..N with wave-wide counts);
-// every chunk below tau is kept, and the first k - #(< tau) chunks equal to
-// tau in index order.
+// wavefront per block; slot i of lane l is chunk 64*i + l, so chunk order is
+// (slot, lane) order and every count is a ballot.  The threshold tau is the
+// smallest df with at least k chunks at or below it (binary search over
+// 1..N); every chunk below tau is kept, and the first k - #(< tau) chunks
+// equal to tau in chunk order.
 __device__ void select_topk(const uint8_t* cmin, int64_t b, int num_blocks, int C, int topk,
                             int32_t* __restrict__ sel, int wave, int lane) {
   if (topk == 0) return;
-  const int per_lane = (C + 63) >> 6;      // contiguous chunks owned by a lane
+  const int slots = (C + 63) >> 6;
   for (int j = wave; j < num_blocks; j += MAXIDF_WAVES) {
     const uint8_t* cv = cmin + (int64_t)j * C;
-    const int c0 = lane * per_lane;
-    const int c1 = min(C, c0 + per_lane);
-    // smallest tau with #(mindf <= tau) >= topk; mindf lies in [1, num_blocks]
-    int lo = 0, hi = num_blocks;
+    // a lane past the last chunk reads 256, above every df (<= 255)
+    auto x_of = [&](int i) { return 64 * i + lane < C ? (int)cv[64 * i + lane] : 256; };
+    int lo = 0, hi = num_blocks;  // #(mindf <= lo) < k <= #(mindf <= hi)
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       int cnt = 0;
-      for (int c = c0; c < c1; ++c) cnt += cv[c] <= mid;
-      cnt = wave_sum_int(cnt);
+      for (int i = 0; i < slots; ++i) cnt += __popcll(__ballot(x_of(i) <= mid));
       if (cnt >= topk) hi = mid; else lo = mid;
     }
     const int tau = hi;
-    int n_lt = 0, n_eq = 0;
-    for (int c = c0; c < c1; ++c) {
-      n_lt += cv[c] < tau;
-      n_eq += cv[c] == tau;
-    }
-    const int need = topk - wave_sum_int(n_lt);  // chunks equal to tau that are kept
-    const int eq_base = wave_excl_scan(n_eq);     // equal-to-tau chunks in lower lanes
-    int n_sel = 0;
-    int r = eq_base;
-    for (int c = c0; c < c1; ++c) {
-      const int x = cv[c];
-      if (x < tau) {
-        ++n_sel;
-      } else if (x == tau) {
-        n_sel += r < need;
-        ++r;
-      }
-    }
-    int out = wave_excl_scan(n_sel);
+    int n_lt = 0;
+    for (int i = 0; i < slots; ++i) n_lt += __popcll(__ballot(x_of(i) < tau));
+    const int need = topk - n_lt;  // chunks equal to tau that are kept
     int32_t* dst = sel + (b * num_blocks + j) * topk;
-    r = eq_base;
-    for (int c = c0; c < c1; ++c) {
-      const int x = cv[c];
-      bool keep = x < tau;
-      if (x == tau) {
-        keep = r < need;
-        ++r;
-      }
-      if (keep) dst[out++] = c;
+    int eq_before = 0, out_before = 0;
+    for (int i = 0; i < slots; ++i) {
+      const int x = x_of(i);
+      const uint64_t m_eq = __ballot(x == tau);
+      const bool keep = x < tau || (x == tau && eq_before + count_below(m_eq) < need);
+      const uint64_t m_keep = __ballot(keep);
+      if (keep) dst[out_before + count_below(m_keep)] = 64 * i + lane;
+      eq_before += __popcll(m_eq);
+      out_before += __popcll(m_keep);
     }
   }
 }
@@ -367,18 +360,20 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
 // also the group pass 2 assigns to iteration 2*rd + u.
 __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
     const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2,
-    int topk, int vocab, int cmin_off, int32_t* __restrict__ sel,
-    int32_t* __restrict__ chunk_mindf, float* __restrict__ idf) {
-  extern __shared__ uint32_t lds[];
+    int topk, int vocab, int32_t* __restrict__ sel, int32_t* __restrict__ chunk_mindf,
+    float* __restrict__ idf) {
+  // A fixed layout in static LDS, whose base the compiler knows, so every
+  // table offset folds into the LDS instructions: two bitmaps, then the df
+  // bytes (vocab <= 131072); the chunk minima (<= 32 KiB) reuse the bitmaps.
+  __shared__ __attribute__((aligned(16))) uint32_t lds[(kResBitmapBytes + kFastVocab) / 4];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t b = blockIdx.x;
   uint8_t* const lds8 = reinterpret_cast<uint8_t*>(lds);
-  uint8_t* df8 = lds8 + kFastBitmapBytes;
+  uint8_t* df8 = lds8 + kResBitmapBytes;
   uint32_t* dfw = reinterpret_cast<uint32_t*>(df8);
-  uint32_t* bits = lds;
-  uint8_t* cmin = lds8 + cmin_off;
+  uint8_t* cmin = lds8;
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const int vocab_w4 = (vocab + 3) >> 2;
   const int4* seq4 = reinterpret_cast<const int4*>(ids + b * L);
@@ -386,6 +381,8 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
   const int rpb = Lb / RES_ROUND_TOKENS;            // rounds per block
 
   for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = 0u;
+  for (int w = tid; w < 2 * kFastWords; w += MAXIDF_THREADS) lds[w] = 0u;
+  __syncthreads();
 
   // ---- pass 1: document frequency, ids kept in registers ------------------
   constexpr int PREFETCH = 2;  // rounds of loads in flight
@@ -402,10 +399,15 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
 #pragma unroll
   for (int rd = 0; rd < RES_ROUNDS; ++rd) {
     if (rd < rounds) {
-      if (rd % rpb == 0) {  // a new block: everyone is done with the previous bitmap
-        __syncthreads();
-        for (int w = tid; w < kFastWords; w += MAXIDF_THREADS) bits[w] = 0u;
-        __syncthreads();
+      // Block j marks bitmap j % 2.  At its start every wave is past block
+      // j-1 (barrier), so the other bitmap is cleared for block j+1 while
+      // this one is marked.
+      const int j = rd / rpb;
+      uint32_t* bits = lds + (j & 1) * kFastWords;
+      if (rd % rpb == 0) {
+        if (rd > 0) __syncthreads();
+        uint32_t* other = lds + ((j + 1) & 1) * kFastWords;
+        for (int w = tid; w < kFastWords; w += MAXIDF_THREADS) other[w] = 0u;
       }
       if (rd + PREFETCH < rounds)
         load_round(rd + PREFETCH, cbuf[(rd + PREFETCH) % (PREFETCH + 1)]);
@@ -468,13 +470,10 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
   while ((1 << chunk_log2) < chunk) ++chunk_log2;
   const MaxidfPlan plan = maxidf_plan(L, num_blocks, chunk, vocab);
   if ((size_t)plan.lds_bytes != lds_bytes) return PULSAR_EINVAL;
-  if (plan.resident) {
-    if (hipFuncSetAttribute((const void*)maxidf_resident_kernel,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes) != hipSuccess)
-      return PULSAR_EHIP;
-    hipLaunchKernelGGL(maxidf_resident_kernel, dim3(batch), dim3(MAXIDF_THREADS), lds_bytes, stream,
-                       ids, L, num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab,
-                       (int)plan.cmin_off, sel, chunk_mindf, idf);
+  if (plan.resident) {  // static LDS only
+    hipLaunchKernelGGL(maxidf_resident_kernel, dim3(batch), dim3(MAXIDF_THREADS), 0, stream, ids,
+                       L, num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, sel,
+                       chunk_mindf, idf);
     return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
   }
   const auto kern = plan.fast ? maxidf_kernel<true> : maxidf_kernel<false>;
