@@ -28,13 +28,13 @@
 //                 and rescales O.  P enters the PV product rounded to bf16; O is
 //                 divided by the sum of those rounded weights (an exact convex
 //                 combination), while the LSE uses the fp32 sum.
-//   O^T += V^T P^T  A = V^T from LDS; B = P, which is already in the
+//   O^T += V^T P^T  A = V^T, read from the V tile (keys as rows) in LDS with
+//                 transposing reads; B = P, which is already in the
 //                 B-operand layout because K rows are stored in LDS with bits
 //                 2 and 3 of the key index swapped.
-//   K tiles move from HBM to LDS by buffer loads that write LDS directly;
-//   V tiles pass through registers and are written transposed.  Three LDS
-//   stages; the K row padding (2d+16 B) keeps the K reads free of bank
-//   conflicts.
+//   K and V tiles move from HBM to LDS by buffer loads that write LDS
+//   directly.  Three LDS stages; the K row padding (2d+16 B) and a chunk
+//   swizzle of the V rows keep the fragment reads free of bank conflicts.
 //   The two wavefronts of a SIMD run ping-pong: one multiplies (PV of the
 //   previous tile, S of the current one) while the other computes weights,
 //   with a workgroup barrier between phases.
@@ -47,22 +47,24 @@ namespace {
 constexpr int BN = 64;          // keys per tile
 constexpr float MAX_SLACK = 8.0f;  // exact pass: log2 slack before the running max is raised
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 constexpr int kBufferFlags = 0x00020000;  // raw 32-bit buffer access (word 3 of the resource)
 __device__ constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 template <int D>
 struct Tile {
   static constexpr int CPR = D / 8;               // 16-byte data chunks per row
   static constexpr int K_CH = CPR + 1;            // K row: data + one pad chunk
   static constexpr int K_STRIDE = 16 * K_CH;      // bytes per K row in LDS
-  static constexpr int V_STRIDE = BN * 2 + 16;    // bytes per V^T row (one head_dim entry)
   static constexpr int K_BYTES = BN * K_STRIDE;   // = K_CH KiB
-  static constexpr int V_BYTES = D * V_STRIDE;
+  static constexpr int V_BYTES = BN * D * 2;      // raw V: rows = keys
   static constexpr int STAGE = K_BYTES + V_BYTES;
-  static constexpr int V_UNITS = (BN / 4) * CPR;  // 4 keys x 8 dims per unit (<= 256)
+  static constexpr int V_SEGS = V_BYTES / 1024;   // 1 KiB load segments of a V tile
   static constexpr int LDS = 3 * STAGE + 3 * BN * 4;  // three stages + three position rows
 };
 
@@ -192,11 +194,14 @@ void attn_fwd_kernel(KernelArgs ka) {
   //   slot 64*sg + l, i.e. row slot / K_CH, chunk slot % K_CH.  K row r holds
   //   key swap_bits23(r).  A pad chunk re-reads chunk 0 of its row, and a key
   //   past the end reads row 0 of the sequence: both finite, never weighted.
-  // V: group-0 thread t (t < V_UNITS) loads keys 4*(t%16) .. +3 at 16-byte
-  //   chunk t/16 into registers and writes them transposed (head_dim-major)
-  //   into LDS, so that the PV product reads V^T fragments with 16-byte
-  //   reads.  A key past the end has position -1, whose offset falls outside
-  //   the buffer resource, so the hardware returns zeros for it.
+  // V: the four group-0 waves move the V tile straight into LDS as well,
+  //   keys as rows (2D bytes each): wave w issues segments w, w+4, ...; lane
+  //   l of segment sg fills chunk position (64 sg + l) % CPR of row
+  //   (64 sg + l) / CPR, which holds 16-byte chunk position ^ vswz(row) of
+  //   that key.  The PV product reads V^T fragments from it with transposing
+  //   reads (v_frag); the chunk swizzle puts the four rows that one 16-lane
+  //   group of such a read touches in disjoint banks.  A key past the end
+  //   reads row 0 of the sequence: finite, and its weight is zero.
   auto tile_positions = [&](int j, int32_t* dst) {
     if (tid < BN) {
       const int k = kv_begin + j * BN + tid;
@@ -226,34 +231,27 @@ void attn_fwd_kernel(KernelArgs ka) {
         lds_dma16(k_rsrc, (uint32_t)max(p[i], 0) * row_bytes + dma_col[i], st_lds + sg * 1024);
     }
   };
-  // group 0 only (V_UNITS <= 256, a multiple of 64: uniform per wave)
-  const bool v_thread = wave * 64 < T::V_UNITS;
-  u32x4 vreg[4];
-  auto load_v = [&](const int32_t* pos) {
-    const int4 p4 = *reinterpret_cast<const int4*>(pos + 4 * (tid & 15));
-    const int vp[4] = {p4.x, p4.y, p4.z, p4.w};
-    const uint32_t vcol = head_off + (uint32_t)(tid >> 4) * 16;
+  constexpr int NVSEG = T::V_SEGS / 4;  // V segments per group-0 wave
+  auto vswz = [](int r) { return (4 * ((r * T::CPR) / 16)) % T::CPR; };
+  int vdma_row[NVSEG];
+  uint32_t vdma_col[NVSEG];
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
-      vreg[rr] = __builtin_amdgcn_raw_buffer_load_b128(v_rsrc, (int)((uint32_t)vp[rr] * row_bytes + vcol),
-                                                       0, 0);
-  };
-  auto store_v = [&](lds_u8* st) {
-    lds_u8* sv = st + T::K_BYTES;
-    const int kq = tid & 15;
-    const int dc = tid >> 4;
+  for (int i = 0; i < NVSEG; ++i) {
+    const int slot = (wave + 4 * i) * 64 + lane;  // meaningful for group 0
+    const int r = (slot / T::CPR) & (BN - 1);
+    vdma_row[i] = r;
+    vdma_col[i] = head_off + (uint32_t)((slot % T::CPR) ^ vswz(r)) * 16;
+  }
+  auto issue_v = [&](const int32_t* pos, lds_u8* st) {
+    const uint32_t st_lds =
+        __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(st + T::K_BYTES));
+    int p[NVSEG];  // all positions first: each asm load orders later LDS reads
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      // head_dim entries 8*dc + 2w (low halves) and 8*dc + 2w + 1 (high halves)
-      const u32x2 lo = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x05040100u),
-                        __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x05040100u)};
-      const u32x2 hi = {__builtin_amdgcn_perm(vreg[1][w], vreg[0][w], 0x07060302u),
-                        __builtin_amdgcn_perm(vreg[3][w], vreg[2][w], 0x07060302u)};
-      *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(
-          sv + (8 * dc + 2 * w) * T::V_STRIDE + 8 * kq) = lo;
-      *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(
-          sv + (8 * dc + 2 * w + 1) * T::V_STRIDE + 8 * kq) = hi;
-    }
+    for (int i = 0; i < NVSEG; ++i) p[i] = pos[vdma_row[i]];
+#pragma unroll
+    for (int i = 0; i < NVSEG; ++i)
+      lds_dma16(v_rsrc, (uint32_t)max(p[i], 0) * row_bytes + vdma_col[i],
+                st_lds + (wave + 4 * i) * 1024);
   };
 
   // ---- building blocks of one 32-key half --------------------------------------
@@ -262,9 +260,27 @@ void attn_fwd_kernel(KernelArgs ka) {
     return *reinterpret_cast<const lds_bf16x8*>(sK + (u * 32 + l32) * T::K_STRIDE +
                                                 (16 * s + 8 * g) * 2);
   };
-  auto v_frag = [&](const lds_u8* sV, int u, int c, int e) {
-    return *reinterpret_cast<const lds_bf16x8*>(sV + (e * 32 + l32) * T::V_STRIDE +
-                                                (u * 32 + 16 * c + 8 * g) * 2);
+  // V^T rows e*32.., keys u*32+16c.. of the tile, as the A operand of PV,
+  // from the raw V tile with two transposing reads.  Within each 16-lane
+  // group such a read hands lane i, for slot j, element i%4 of the four that
+  // lane 4j + i/4 addressed; so lane 16a + 4j + q addresses key row
+  // 8(a/2) + j (+4 for the second read) at head_dim 16(a%2) + 4q, and lane
+  // 16a + i receives head_dim 16(a%2) + i of keys 8(a/2) .. +7.
+  uint32_t vtr_base[DT];
+  {
+    const int a16 = lane >> 4, j = (lane >> 2) & 3, q = lane & 3;
+    const int trow = 8 * (a16 >> 1) + j;  // vswz of every row read equals vswz(trow)
+    const int cb = 2 * (a16 & 1) + (q >> 1);
+#pragma unroll
+    for (int e = 0; e < DT; ++e)
+      vtr_base[e] = trow * (2 * D) + 16 * ((4 * e + cb) ^ vswz(trow)) + 8 * (q & 1);
+  }
+  auto v_frag = [&](const lds_u8* sV, int u, int c, int e) -> bf16x8 {
+    const lds_u8* b = sV + vtr_base[e] + (u * 32 + 16 * c) * (2 * D);
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)b);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(b + 4 * (2 * D)));
+    return __builtin_bit_cast(bf16x8,
+                              (s16x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
   };
 
 
@@ -340,11 +356,12 @@ void attn_fwd_kernel(KernelArgs ka) {
   //
   // Tiles rotate through three LDS stages (tile t in stage t % 3).  Tile t's
   // K is read in phases 2t and 2t+1 of the workgroup (S by group 0, then by
-  // group 1) and its V^T in phases 2t+2 and 2t+3 (PV).  Group 1 moves K_t
+  // group 1) and its V in phases 2t+2 and 2t+3 (PV).  Group 1 moves K_t
   // into LDS during its V_{t-2} and waits for it at the end of its M_{t-1};
-  // group 0 loads V_t into registers during V_{t-1} and writes V^T_t during
-  // V_t.  Stage t % 3 last held tile t-3, whose last reader ran before
-  // either write.  Wave 0 writes tile t's key positions during V_{t-2}.
+  // group 0 moves V_t into LDS during its V_{t-1} and waits for it at the end
+  // of its V_t.  Stage t % 3 last held tile t-3, whose last reader ran before
+  // either load was issued.  Wave 0 writes tile t's key positions during
+  // V_{t-2}.
   static_assert(WAVES == 8, "the ping-pong schedule pairs waves w and w+4 on one SIMD");
   const int grp = wave >> 2;
   // The stage offset goes through readfirstlane so that loop strength
@@ -417,7 +434,7 @@ void attn_fwd_kernel(KernelArgs ka) {
     __syncthreads();
     if (ntiles > 0) {
       if (grp == 1) issue_k(pos_of(0), stage_of(0));
-      if (v_thread) load_v(pos_of(0));
+      if (grp == 0) issue_v(pos_of(0), stage_of(0));
     }
     if (ntiles > 1) tile_positions(1, pos_of(1));
     if (grp == 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -451,10 +468,7 @@ void attn_fwd_kernel(KernelArgs ka) {
     // fully masked and weighs zero).
     auto v_phase = [&](int m) {
       if (grp == 1 && m + 2 < ntiles) issue_k(pos_of(m + 2), stage_of(m + 2));
-      if (v_thread) {  // V^T of tile m into its stage, then V of tile m+1 into registers
-        store_v(stage_of(m));
-        if (m + 1 < ntiles) load_v(pos_of(m + 1));
-      }
+      if (grp == 0 && m + 1 < ntiles) issue_v(pos_of(m + 1), stage_of(m + 1));
       if (m + 2 < ntiles) tile_positions(m + 2, pos_of(m + 2));  // wave 0
 #pragma unroll
       for (int u = 0; u < 2; ++u)
@@ -482,9 +496,15 @@ void attn_fwd_kernel(KernelArgs ka) {
       }
       weights(S[0], P[0]);
       weights(S[1], P[1]);
+      // V of tile m must be in LDS for M_{m+1}; only V of tile m+1 may still
+      // be in flight.
+      if (grp == 0) {
+        if (m + 1 < ntiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NVSEG) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      }
       phase_barrier();
     };
-    // Every matrix phase is the full one: M_0 multiplies the zeroed V^T of
+    // Every matrix phase is the full one: M_0 multiplies the zeroed V of
     // stage 2 by P = 0, and M_ntiles computes an S that is never used (from
     // finite LDS data).
     for (int m = 0; m <= ntiles; ++m) {
