@@ -25,6 +25,9 @@ Modules, each following the paper's definitions in its own notation:
                    dense attention over all keys.
 * ``cost``      -- the Phase-1 cost model (Table 4; Appendix "Block-to-Host
                    Scalability Analysis").
+* ``rope``      -- rotary position embedding of query/key rows at their
+                   preserved global positions (Appendix "RoPE Position ID
+                   Assignment", sparse mode).
 
 Readings of points the paper leaves open are listed in each function's
 docstring.
