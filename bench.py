@@ -206,6 +206,21 @@ def run_main(args):
     torch.cuda.synchronize()
     del big
 
+    # Rotary embedding of the layer's Q and K at their global positions (the
+    # sparse-position mode), once per layer for the whole context; on copies,
+    # so that the attention inputs above stay as drawn
+    t_rope = Timer()
+    Qr, Kr = Q.clone(), K.clone()
+    P.rope_(Qr)
+    P.rope_(Kr)
+    for _ in range(5):
+        with t_rope:
+            P.rope_(Qr)
+            P.rope_(Kr)
+    torch.cuda.synchronize()
+    rope_bytes = 2 * (Qr.numel() + Kr.numel()) * 2
+    del Qr, Kr
+
     f_p1 = causal_flops(n, cfg.Hq, cfg.d)
     f_star = causal_flops(n_star, cfg.Hq, cfg.d)
     f_p2 = full_flops(Tq, N * cfg.Lb, cfg.Hq, cfg.d)
@@ -247,6 +262,11 @@ def run_main(args):
                 "gbps_algorithmic": IDF_THROUGHPUT_BATCH * idf_bytes / (t_idf_big.mean_ms() * 1e-3) / 1e9,
                 "pct_hbm_peak": 100 * IDF_THROUGHPUT_BATCH * idf_bytes / (t_idf_big.mean_ms() * 1e-3)
                                 / 1e9 / PEAK_HBM_GBPS,
+            },
+            "rope_qk": {
+                "ms": t_rope.mean_ms(),
+                "gbps_algorithmic": rope_bytes / (t_rope.mean_ms() * 1e-3) / 1e9,
+                "pct_hbm_peak": 100 * rope_bytes / (t_rope.mean_ms() * 1e-3) / 1e9 / PEAK_HBM_GBPS,
             },
             "phase2_partial_merge_ms": p2_ms,
             "phase2_tflops": f_p2 / (p2_ms * 1e-3) / 1e12,

@@ -204,6 +204,33 @@ int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_sha
 int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq, int Hq,
                      int d, float* o, float* lse, void* stream);
 
+/*
+ * Rotary position embedding of query or key rows at given positions
+ * (Appendix "RoPE Position ID Assignment").  In the paper's sparse mode every
+ * token keeps its global position id, so rotating a layer's Q and K of the
+ * whole context once, by position, gives every block's Phase-1 input (and
+ * the retained KV) its rotated rows; pulsar_phase1_attn then reads them.
+ *
+ * Rotate-half form: for a head vector x of width d, pair i < d/2 is
+ * (x_i, x_{i+d/2}) and becomes
+ *   (x_i cos(p w_i) - x_{i+d/2} sin(p w_i),  x_{i+d/2} cos(p w_i) + x_i sin(p w_i))
+ * for the row's position p.  The angle is formed in fp64 and reduced to
+ * [-pi, pi]; the rotation is evaluated in fp32 and rounded once to bf16.
+ *
+ * X         bf16 [batch, n_rows, H, d], 16-byte aligned, rotated in place.
+ * pos       int32 [batch, n_rows]: the rows' positions; NULL means the row
+ *           index within its sequence.  pos_offset is added to every
+ *           position (for example the first position of Phase-2 queries).
+ * inv_freq  HOST pointer to d/2 floats, the frequencies w_i (a model's
+ *           scaled table); NULL means w_i = base^(-2i/d).
+ *
+ * EINVAL: negative sizes, NULL or misaligned X when there is work, odd d,
+ *         a non-finite table entry, or (without a table) base not finite
+ *         and > 0.  EUNSUPPORTED: d not in {64, 128}.
+ */
+int pulsar_rope(void* X, int batch, int64_t n_rows, int H, int d, const int32_t* pos,
+                int64_t pos_offset, const float* inv_freq, double base, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,6 +6,7 @@ computation happens in the HIP kernels behind ``libpulsar.so``.
 """
 from __future__ import annotations
 
+import ctypes
 import math
 
 import torch
@@ -166,3 +167,28 @@ def lse_merge(o_parts, lse_parts):
                                      _ptr(lse), _stream())
     _lib.check(st, "pulsar_lse_merge")
     return o, lse
+
+
+def rope_(x, pos=None, pos_offset: int = 0, inv_freq=None, base: float = 500000.0):
+    """Rotate x bf16 [batch, n, H, d] (or [n, H, d]) in place by the rows'
+    positions: pos int32 [batch, n] (None: row index) plus pos_offset.
+    inv_freq: the d/2 frequencies (a host sequence of floats), or None for
+    base^(-2i/d).  Returns x."""
+    _need(x, torch.bfloat16, "x")
+    xv = x[None] if x.dim() == 3 else x
+    batch, n, H, d = xv.shape
+    if pos is not None:
+        _need(pos, torch.int32, "pos")
+        if pos.numel() != batch * n:
+            raise ValueError("pos must hold one position per row")
+    table = None
+    if inv_freq is not None:
+        vals = [float(v) for v in (inv_freq.tolist() if hasattr(inv_freq, "tolist") else inv_freq)]
+        if len(vals) != d // 2:
+            raise ValueError("inv_freq must hold d/2 values")
+        table = (ctypes.c_float * len(vals))(*vals)
+    st = _lib.lib().pulsar_rope(_ptr(xv), batch, n, H, d, _ptr(pos), int(pos_offset),
+                                None if table is None else ctypes.cast(table, ctypes.c_void_p),
+                                float(base), _stream())
+    _lib.check(st, "pulsar_rope")
+    return x

@@ -1,0 +1,138 @@
+// Rotary position embedding of query/key rows at given positions (Appendix
+// "RoPE Position ID Assignment").  In the paper's sparse mode every token
+// keeps its global position id, so one pass over a layer's Q and K of the
+// whole context gives every block's Phase-1 input its rotated rows: the
+// rotation of a row depends on its position alone, not on the block whose
+// input it appears in.
+//
+// Rotate-half form: pair i < d/2 of a head vector is (x_i, x_{i+d/2}) and is
+// turned by the angle p * w_i.
+//
+// Thread (row, j) owns pairs 8j .. 8j+7 of every head of its row: 16-byte
+// loads of x[8j .. 8j+7] and x[d/2+8j .. d/2+8j+7].  Its eight angles are
+// formed once, in fp64 (p * w_i, then reduced to [-pi, pi] with a two-part
+// 2*pi), and their sine and cosine (fp32, on the reduced angle) serve every
+// head of the row.  The rotation is evaluated in fp32 and rounded once to
+// bf16.  Bound by HBM: 2 * n_rows * H * d * 2 bytes per call.
+#include <cmath>
+
+#include "common.hpp"
+
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kRopeThreads = 256;
+constexpr int kMaxHalf = 64;  // d <= 128
+
+struct RopeFreqs {
+  double w[kMaxHalf];  // w_i, i < d/2
+};
+
+// 2*pi split into a double and the double nearest its remainder.
+constexpr double kTwoPiHi = 6.283185307179586;
+constexpr double kTwoPiLo = 2.4492935982947064e-16;
+constexpr double kInvTwoPi = 0.15915494309189535;
+
+template <int D>
+__global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict__ X,
+                                                            int64_t rows, int64_t n_rows, int H,
+                                                            const int32_t* __restrict__ pos,
+                                                            int64_t pos_offset, RopeFreqs f) {
+  constexpr int G = D / 16;  // threads per row
+  const int64_t t = (int64_t)blockIdx.x * kRopeThreads + threadIdx.x;
+  const int64_t row = t / G;
+  const int j = (int)(t % G);
+  if (row >= rows) return;
+  const int64_t p = (pos ? (int64_t)pos[row] : row % n_rows) + pos_offset;
+  const double pd = (double)p;
+  float c[8], s[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    const double a = pd * f.w[8 * j + v];
+    const double k = rint(a * kInvTwoPi);
+    double r = fma(-k, kTwoPiHi, a);
+    r = fma(-k, kTwoPiLo, r);
+    sincosf((float)r, &s[v], &c[v]);
+  }
+  uint16_t* base = X + row * (int64_t)H * D + 8 * j;
+  auto rotate = [&](const u32x4 lo, const u32x4 hi, u32x4& olo, u32x4& ohi) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      // words hold elements 2w (low half) and 2w+1 (high half)
+      const float x0a = __builtin_bit_cast(float, lo[w] << 16);
+      const float x0b = __builtin_bit_cast(float, lo[w] & 0xffff0000u);
+      const float x1a = __builtin_bit_cast(float, hi[w] << 16);
+      const float x1b = __builtin_bit_cast(float, hi[w] & 0xffff0000u);
+      const int va = 2 * w, vb = 2 * w + 1;
+      const f32x2 ylo = {fmaf(x0a, c[va], -x1a * s[va]), fmaf(x0b, c[vb], -x1b * s[vb])};
+      const f32x2 yhi = {fmaf(x1a, c[va], x0a * s[va]), fmaf(x1b, c[vb], x0b * s[vb])};
+      olo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(ylo, bf16x2));
+      ohi[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(yhi, bf16x2));
+    }
+  };
+  // four heads at a time: all eight loads in flight before the first store
+  constexpr int U = 4;
+  int h = 0;
+  for (; h + U <= H; h += U) {
+    u32x4 lo[U], hi[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      lo[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)(h + u) * D);
+      hi[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)(h + u) * D + D / 2);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      u32x4 olo, ohi;
+      rotate(lo[u], hi[u], olo, ohi);
+      *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D) = olo;
+      *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D + D / 2) = ohi;
+    }
+  }
+  for (; h < H; ++h) {
+    u32x4* plo = reinterpret_cast<u32x4*>(base + (int64_t)h * D);
+    u32x4* phi = reinterpret_cast<u32x4*>(base + (int64_t)h * D + D / 2);
+    u32x4 olo, ohi;
+    rotate(*plo, *phi, olo, ohi);
+    *plo = olo;
+    *phi = ohi;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int pulsar_rope(void* X, int batch, int64_t n_rows, int H, int d, const int32_t* pos,
+                int64_t pos_offset, const float* inv_freq, double base, void* stream) {
+  if (batch < 0 || n_rows < 0 || H < 0) return PULSAR_EINVAL;
+  if (d != 64 && d != 128) return d > 0 && d % 2 == 0 ? PULSAR_EUNSUPPORTED : PULSAR_EINVAL;
+  const int64_t rows = (int64_t)batch * n_rows;
+  if (rows == 0 || H == 0) return PULSAR_OK;
+  if (X == nullptr || (reinterpret_cast<uintptr_t>(X) & 15u) != 0) return PULSAR_EINVAL;
+  RopeFreqs f{};
+  if (inv_freq) {
+    for (int i = 0; i < d / 2; ++i) {
+      if (!std::isfinite(inv_freq[i])) return PULSAR_EINVAL;
+      f.w[i] = (double)inv_freq[i];
+    }
+  } else {
+    if (!(base > 0.0) || !std::isfinite(base)) return PULSAR_EINVAL;
+    for (int i = 0; i < d / 2; ++i) f.w[i] = std::pow(base, -2.0 * i / d);
+  }
+  const int G = d / 16;
+  const int64_t threads = rows * G;
+  const int64_t blocks = (threads + kRopeThreads - 1) / kRopeThreads;
+  if (blocks > 0x7fffffff) return PULSAR_EUNSUPPORTED;
+  auto s = (hipStream_t)stream;
+  if (d == 128)
+    hipLaunchKernelGGL(rope_kernel<128>, dim3((unsigned)blocks), dim3(kRopeThreads), 0, s,
+                       (uint16_t*)X, rows, n_rows, H, pos, pos_offset, f);
+  else
+    hipLaunchKernelGGL(rope_kernel<64>, dim3((unsigned)blocks), dim3(kRopeThreads), 0, s,
+                       (uint16_t*)X, rows, n_rows, H, pos, pos_offset, f);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+}  // extern "C"

@@ -137,3 +137,22 @@ def test_binding_refuses_missing_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError):
         _lib.lib()
+
+
+def test_rope_validation():
+    f = _lib.lib().pulsar_rope
+    table = (ctypes.c_float * 64)(*([1.0] * 64))
+    def call(X=FAKE, batch=1, n=4, H=2, d=128, pos=None, off=0, tab=None, base=500000.0):
+        return f(X, batch, n, H, d, pos, off, tab, base, None)
+    assert call(batch=-1) == EINVAL
+    assert call(n=-1) == EINVAL
+    assert call(d=63) == EINVAL
+    assert call(d=32) == EUNSUP
+    assert call(X=None) == EINVAL
+    assert call(X=FAKE + 8) == EINVAL      # misaligned
+    assert call(base=0.0) == EINVAL
+    assert call(base=float("inf")) == EINVAL
+    bad = (ctypes.c_float * 64)(*([1.0] * 63 + [float("nan")]))
+    assert call(tab=ctypes.cast(bad, ctypes.c_void_p)) == EINVAL
+    assert call(n=0) == 0 and call(X=None, batch=0) == 0   # nothing to do
+    del table
