@@ -153,3 +153,29 @@ def lse_merge(o_parts, lse_parts):
 def dense_attention(q, K, V, scale: float):
     """Unmasked attention over all keys at once (the Phase-2 reference)."""
     return partial_attention(q, K, V, scale)
+
+
+def query_attention(q, K_shards, V_shards, Kg, Vg, G: int, scale: float):
+    """Phase-2 attention of Tq new tokens (Algorithm 1, Phase 2).
+
+    The retained shards K_shards/V_shards [H, S, Hkv, d] are all visible; the
+    designated generation shard's appended rows Kg/Vg [G + Tq, Hkv, d] hold G
+    earlier query/generated tokens, then the Tq new ones, and new token t sees
+    appended rows 0 .. G + t (itself included).  Each token's softmax is taken
+    over exactly the keys it sees, concatenated: (o [Tq, Hq, d], lse [Hq, Tq]).
+
+    Reading: Algorithm 1 appends every query and generated token's KV to one
+    designated shard; a token sees the tokens before it and itself there."""
+    q = _f64(q)
+    Kc = np.concatenate([_f64(K_shards).reshape(-1, *K_shards.shape[2:]), _f64(Kg)], axis=0)
+    Vc = np.concatenate([_f64(V_shards).reshape(-1, *V_shards.shape[2:]), _f64(Vg)], axis=0)
+    n_ctx = Kc.shape[0] - Kg.shape[0]
+    Tq, Hq, d = q.shape
+    o = np.zeros((Tq, Hq, d))
+    lse = np.zeros((Hq, Tq))
+    for t in range(Tq):
+        vis = n_ctx + G + t + 1
+        ot, lt = partial_attention(q[t:t + 1], Kc[:vis], Vc[:vis], scale)
+        o[t] = ot[0]
+        lse[:, t] = lt[:, 0]
+    return o, lse
