@@ -221,6 +221,25 @@ def run_main(args):
     rope_bytes = 2 * (Qr.numel() + Kr.numel()) * 2
     del Qr, Kr
 
+    # Phase 2 of new tokens over the 16 retained shards: the 64-token query
+    # encoding (its own rows causally), and one decode step (1 token after 64)
+    kg = bf16_dev(workload.bf16_normal(cfg.seed * 10 + 8, (Tq + 1, cfg.Hkv, cfg.d)))
+    vg = bf16_dev(workload.bf16_normal(cfg.seed * 10 + 9, (Tq + 1, cfg.Hkv, cfg.d)))
+    shards_k = K[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
+    shards_v = V[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
+    q_dec = q_dev[:1].contiguous()
+    t_enc, t_dec = Timer(), Timer()
+    for _ in range(2):
+        P.phase2_query(q_dev, kg[:Tq], vg[:Tq], 0, shards_k, shards_v)
+        P.phase2_query(q_dec, kg, vg, Tq, shards_k, shards_v)
+    for _ in range(5):
+        with t_enc:
+            P.phase2_query(q_dev, kg[:Tq], vg[:Tq], 0, shards_k, shards_v)
+        with t_dec:
+            P.phase2_query(q_dec, kg, vg, Tq, shards_k, shards_v)
+    torch.cuda.synchronize()
+    kv_bytes = 2 * N * cfg.Lb * cfg.Hkv * cfg.d * 2
+
     f_p1 = causal_flops(n, cfg.Hq, cfg.d)
     f_star = causal_flops(n_star, cfg.Hq, cfg.d)
     f_p2 = full_flops(Tq, N * cfg.Lb, cfg.Hq, cfg.d)
@@ -267,6 +286,12 @@ def run_main(args):
                 "ms": t_rope.mean_ms(),
                 "gbps_algorithmic": rope_bytes / (t_rope.mean_ms() * 1e-3) / 1e9,
                 "pct_hbm_peak": 100 * rope_bytes / (t_rope.mean_ms() * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+            },
+            "phase2_query": {
+                "encoding_tq64_ms": t_enc.mean_ms(),
+                "decode_step_ms": t_dec.mean_ms(),
+                "decode_kv_gbps": kv_bytes / (t_dec.mean_ms() * 1e-3) / 1e9,
+                "decode_pct_hbm_peak": 100 * kv_bytes / (t_dec.mean_ms() * 1e-3) / 1e9 / PEAK_HBM_GBPS,
             },
             "phase2_partial_merge_ms": p2_ms,
             "phase2_tflops": f_p2 / (p2_ms * 1e-3) / 1e12,

@@ -205,6 +205,39 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
                      int d, float* o, float* lse, void* stream);
 
 /*
+ * Phase-2 attention of new tokens (Algorithm 1, Phase 2: the query encoding
+ * and every generation step).  Every query and generated token's KV is
+ * appended to one designated generation shard; a new token attends, without
+ * a mask, to all retained shards (KV_h after Phase 1) and to the appended
+ * rows before it, and to itself.  Computed as the shard partials (as in
+ * pulsar_phase2_partial), a partial over the G earlier appended rows, an
+ * index-causal partial over the Tq new tokens' own rows, and one
+ * online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
+ *
+ * q         bf16 [Tq, Hq, d]: the new tokens' queries.
+ * Kg, Vg    bf16 [G + Tq, Hkv, d]: the generation shard's appended rows, the
+ *           G earlier tokens first, then the Tq new tokens' own keys/values.
+ * K, V      bf16 [n_shards, S, Hkv, d]: the retained shards (nullable when
+ *           n_shards == 0 or S == 0).
+ * o         out float32 [Tq, Hq, d];  lse out float32 [Hq, Tq], nullable.
+ * workspace device buffer of at least pulsar_phase2_query_workspace_bytes
+ *           bytes, 16-byte aligned; contents on entry do not matter.
+ * Query encoding: G = 0, Tq = query length.  Decode step: Tq = 1, G = the
+ * number of query and generated tokens before it.
+ *
+ * EINVAL: negative sizes, Hq % Hkv != 0, NULL required pointers, misaligned
+ *         buffers, scale not finite and > 0.  EWORKSPACE: workspace NULL,
+ *         misaligned or too small.
+ * EUNSUPPORTED: d not in {64, 128}; Hq / Hkv not 1, 2 or a multiple of 4.
+ */
+size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int64_t G, int Hq,
+                                           int Hkv, int d);
+int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
+                        const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
+                        float softmax_scale, float* o, float* lse, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/*
  * Rotary position embedding of query or key rows at given positions
  * (Appendix "RoPE Position ID Assignment").  In the paper's sparse mode every
  * token keeps its global position id, so rotating a layer's Q and K of the

@@ -171,11 +171,17 @@ def query_attention(q, K_shards, V_shards, Kg, Vg, G: int, scale: float):
     Vc = np.concatenate([_f64(V_shards).reshape(-1, *V_shards.shape[2:]), _f64(Vg)], axis=0)
     n_ctx = Kc.shape[0] - Kg.shape[0]
     Tq, Hq, d = q.shape
+    group = Hq // Kc.shape[1]
+    # key c is visible to token t iff c <= n_ctx + G + t
+    visible = np.arange(Kc.shape[0])[None, :] <= (n_ctx + G + np.arange(Tq))[:, None]
     o = np.zeros((Tq, Hq, d))
     lse = np.zeros((Hq, Tq))
-    for t in range(Tq):
-        vis = n_ctx + G + t + 1
-        ot, lt = partial_attention(q[t:t + 1], Kc[:vis], Vc[:vis], scale)
-        o[t] = ot[0]
-        lse[:, t] = lt[:, 0]
+    for h in range(Hq):
+        g = h // group
+        s = np.where(visible, (q[:, h] @ Kc[:, g].T) * scale, -np.inf)   # [Tq, n_keys]
+        mx = s.max(axis=1, keepdims=True)
+        p = np.exp(s - mx)
+        den = p.sum(axis=1, keepdims=True)
+        o[:, h] = (p @ Vc[:, g]) / den
+        lse[h] = (mx + np.log(den))[:, 0]
     return o, lse

@@ -6,4 +6,4 @@ The computation lives in ``libpulsar.so`` (HIP kernels behind the C ABI of
 """
 from .api import (OUT_BF16, OUT_F32, PREFIX_ANCHOR, PREFIX_SUMMARY, lse_merge,  # noqa: F401
                   maxidf_summaries, phase1_attn, phase1_len, phase1_positions, phase2_partial,
-                  phase2_workspace_bytes, rope_)
+                  phase2_query, phase2_workspace_bytes, rope_)

@@ -192,3 +192,37 @@ def rope_(x, pos=None, pos_offset: int = 0, inv_freq=None, base: float = 500000.
                                 float(base), _stream())
     _lib.check(st, "pulsar_rope")
     return x
+
+
+def phase2_query(q, Kg, Vg, G: int, K=None, V=None, softmax_scale: float | None = None,
+                 workspace=None):
+    """Attention of Tq new tokens: q bf16 [Tq, Hq, d] over the retained
+    shards K/V bf16 [n_shards, S, Hkv, d] (or None) and the generation shard's
+    appended rows Kg/Vg bf16 [G + Tq, Hkv, d] up to each token itself
+    -> (o f32 [Tq, Hq, d], lse f32 [Hq, Tq])."""
+    _need(q, torch.bfloat16, "q")
+    _need(Kg, torch.bfloat16, "Kg")
+    _need(Vg, torch.bfloat16, "Vg")
+    Tq, Hq, d = q.shape
+    Hkv = Kg.shape[1]
+    if Kg.shape != (G + Tq, Hkv, d) or Vg.shape != Kg.shape:
+        raise ValueError("Kg/Vg must be [G + Tq, Hkv, d]")
+    n_shards, S = 0, 0
+    if K is not None:
+        _need(K, torch.bfloat16, "K")
+        _need(V, torch.bfloat16, "V")
+        n_shards, S = K.shape[0], K.shape[1]
+        if K.shape != (n_shards, S, Hkv, d) or V.shape != K.shape:
+            raise ValueError("K/V must be [n_shards, S, Hkv, d]")
+    scale = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
+    dev = q.device
+    o = torch.empty((Tq, Hq, d), dtype=torch.float32, device=dev)
+    lse = torch.empty((Hq, Tq), dtype=torch.float32, device=dev)
+    need = _lib.lib().pulsar_phase2_query_workspace_bytes(n_shards, Tq, S, G, Hq, Hkv, d)
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    st = _lib.lib().pulsar_phase2_query(_ptr(q), _ptr(Kg), _ptr(Vg), G, _ptr(K), _ptr(V), n_shards,
+                                        Tq, S, Hq, Hkv, d, scale, _ptr(o), _ptr(lse),
+                                        _ptr(workspace), need, _stream())
+    _lib.check(st, "pulsar_phase2_query")
+    return o, lse

@@ -1,6 +1,8 @@
 // C ABI entry points: host-side validation, then kernel launches.
 #include <math.h>
 
+#include <algorithm>
+
 #include "common.hpp"
 
 namespace {
@@ -268,6 +270,97 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
   if (!aligned16(o_parts) || !aligned16(o)) return PULSAR_EINVAL;
   return launch_lse_merge(o_parts, lse_parts, H, 1, Tq, Hq, d, (int64_t)Tq * Hq * d,
                           (int64_t)Hq * Tq, o, lse, (hipStream_t)stream);
+}
+
+// Phase-2 attention of new tokens: partials of the shards, of the G earlier
+// appended rows and of the new tokens' own rows (causal), then one merge.
+// Workspace: the partials (o, then lse, each 16-byte aligned), then the key
+// split space of the shard pass (the larger of the two unmasked passes).
+namespace {
+inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
+int query_parts(int n_shards, int64_t G) { return n_shards + (G > 0 ? 1 : 0) + 1; }
+}  // namespace
+
+size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int64_t G, int Hq,
+                                           int Hkv, int d) {
+  if (n_shards < 0 || Tq < 0 || S < 0 || G < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1)
+    return 0;
+  const size_t parts = (size_t)query_parts(n_shards, G);
+  const size_t po = align16(parts * Tq * Hq * d * 4), pl = align16(parts * Hq * Tq * 4);
+  const size_t split = std::max(pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d),
+                                pulsar_phase2_workspace_bytes(1, Tq, G, Hq, Hkv, d));
+  return po + pl + split;
+}
+
+int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
+                        const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
+                        float softmax_scale, float* o, float* lse, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (n_shards < 0 || Tq < 0 || S < 0 || G < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1)
+    return PULSAR_EINVAL;
+  if (!(softmax_scale > 0.f) || !isfinite(softmax_scale)) return PULSAR_EINVAL;
+  if (d != 64 && d != 128) return PULSAR_EUNSUPPORTED;
+  if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
+  if (G + Tq >= PULSAR_MAX_ROWS || (G + Tq) * Hkv * d * 2 >= ((int64_t)1 << 31))
+    return PULSAR_EUNSUPPORTED;
+  if (Tq == 0) return PULSAR_OK;
+  if (q == nullptr || Kg == nullptr || Vg == nullptr || o == nullptr) return PULSAR_EINVAL;
+  if (n_shards > 0 && S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;
+  if (!aligned16(q) || !aligned16(Kg) || !aligned16(Vg) || !aligned16(o)) return PULSAR_EINVAL;
+  const size_t need = pulsar_phase2_query_workspace_bytes(n_shards, Tq, S, G, Hq, Hkv, d);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return PULSAR_EWORKSPACE;
+
+  const int parts = query_parts(n_shards, G);
+  const int64_t ostride = (int64_t)Tq * Hq * d, lstride = (int64_t)Hq * Tq;
+  float* po = static_cast<float*>(workspace);
+  float* pl = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                       align16((size_t)parts * ostride * 4));
+  char* split = reinterpret_cast<char*>(pl) + align16((size_t)parts * lstride * 4);
+  const size_t split_bytes = need - (size_t)(split - static_cast<char*>(workspace));
+  int part = 0, st = PULSAR_OK;
+  if (n_shards > 0) {  // parts 0 .. n_shards-1
+    st = pulsar_phase2_partial(q, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, po, pl, split,
+                               split_bytes, stream);
+    if (st != PULSAR_OK) return st;
+    part = n_shards;
+  }
+  if (G > 0) {  // the earlier appended rows, all visible
+    st = pulsar_phase2_partial(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, po + part * ostride,
+                               pl + part * lstride, split, split_bytes, stream);
+    if (st != PULSAR_OK) return st;
+    ++part;
+  }
+  // the new tokens' own rows: index-causal, square
+  const int64_t row = (int64_t)Hkv * d;
+  AttnLaunch a{};
+  a.Q = static_cast<const uint16_t*>(q);
+  a.K = static_cast<const uint16_t*>(Kg) + G * row;
+  a.V = static_cast<const uint16_t*>(Vg) + G * row;
+  a.q_zstride = 0;
+  a.kv_zstride = Tq * row;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.d = d;
+  a.n_q = Tq;
+  a.n_kv = Tq;
+  a.causal = 1;
+  a.nsplit = 1;
+  a.split_len = Tq;
+  a.nz_kv = 1;
+  a.map = RowMap{};
+  a.map.mode = MAP_IDENTITY;
+  a.sel = nullptr;
+  a.scale_log2 = softmax_scale * 1.4426950408889634f;
+  a.O = po + part * ostride;
+  a.o_bf16 = 0;
+  a.o_zstride = ostride;
+  a.lse = pl + part * lstride;
+  a.lse_zstride = lstride;
+  st = launch_attention(a, (hipStream_t)stream);
+  if (st != PULSAR_OK) return st;
+  return launch_lse_merge(po, pl, parts, 1, Tq, Hq, d, ostride, lstride, o, lse,
+                          (hipStream_t)stream);
 }
 
 }  // extern "C"

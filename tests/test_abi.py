@@ -156,3 +156,24 @@ def test_rope_validation():
     assert call(tab=ctypes.cast(bad, ctypes.c_void_p)) == EINVAL
     assert call(n=0) == 0 and call(X=None, batch=0) == 0   # nothing to do
     del table
+
+
+def test_phase2_query_validation():
+    lib = _lib.lib()
+    f = lib.pulsar_phase2_query
+    ws_need = lib.pulsar_phase2_query_workspace_bytes(4, 8, 1024, 3, 32, 8, 128)
+    assert ws_need > 0
+    def call(q=FAKE, kg=FAKE, vg=FAKE, G=3, K=FAKE, V=FAKE, ns=4, Tq=8, S=1024, Hq=32, Hkv=8,
+             d=128, scale=0.088, o=FAKE, ws=FAKE, wsb=None):
+        return f(q, kg, vg, G, K, V, ns, Tq, S, Hq, Hkv, d, scale, o, None, ws,
+                 ws_need if wsb is None else wsb, None)
+    assert call(G=-1) == EINVAL
+    assert call(Hq=30) == EINVAL           # Hq % Hkv
+    assert call(scale=0.0) == EINVAL
+    assert call(kg=None) == EINVAL
+    assert call(o=None) == EINVAL
+    assert call(q=FAKE + 4) == EINVAL      # misaligned
+    assert call(d=96) == EUNSUP
+    assert call(ws=None) == EWS
+    assert call(wsb=ws_need - 1) == EWS
+    assert call(Tq=0) == 0
