@@ -5,24 +5,34 @@
 // table of that sequence in the compute unit's local data share (LDS), so the
 // table never touches HBM:
 //
-//   pass 1  for every block j: clear a vocab-sized bitmap, stream the block's
-//           ids with 16-byte loads, atomically set each id's bit; the thread
-//           that sets a bit first adds one to that id's df byte (df <= 255).
+//   pass 1  the blocks in order, a workgroup barrier between two blocks:
+//           stream the block's ids with 16-byte loads and count each id once
+//           per block in its df entry.
 //   pass 2  look up the df of every id; lanes of one chunk (chunk/4 lanes)
 //           take the minimum with cross-lane operations.  The chunk minima go
 //           to LDS (and optionally to HBM).
 //   select  one wavefront per block picks the top-k chunks (select_topk).
 //
-// Three variants share these steps:
-//   * general  (any vocab that fits): df bytes, then a scattered bitmap;
+// Pass 1 counts "once per block" in one of two ways:
+//   * stamp code (N <= 16): one byte per id holds its df so far and the last
+//     block it was seen in (see stamp_tokens).  A lane reads the byte and,
+//     if the id is not yet stamped with the current block, writes the code of
+//     (df + 1, this block).  Every lane that writes an id's byte during one
+//     block writes the same value, so plain byte loads and stores suffice: no
+//     atomics, and nothing to clear between blocks.
+//   * bitmaps (any N <= 255): a per-block bitmap, set with atomic OR; the
+//     lane that sets a bit first adds one to the id's df byte.
+//
+// Three kernels:
+//   * resident (vocab <= 131072, L = 8192 times a power of two up to 16,
+//     blocks of a multiple of 8192 ids, hence N <= 16): stamp code; pass 1
+//     keeps every thread's ids (up to 128) in registers, packed, and pass 2
+//     reads them back from there, so the ids cross HBM once; persistent over
+//     the batch, one workgroup per compute unit;
+//   * streaming, stamp code (N <= 16, table and chunk minima fit in LDS):
 //     pass 2 streams the ids from HBM a second time;
-//   * compact  (vocab <= 131072): a fixed 4096-word bitmap whose word is
-//     t & 4095 (the most frequent, low ids spread over all banks) and the df
-//     bytes behind it; pass 2 streams the ids again;
-//   * resident (compact, L <= 131072, blocks of a multiple of 8192 ids): pass
-//     1 keeps every thread's 128 ids in registers, packed, and pass 2 reads
-//     them back from there, so the ids cross HBM once; two bitmaps alternate
-//     between blocks, one barrier per block.
+//   * streaming, bitmaps: compact layout (vocab <= 131072: a fixed 4096-word
+//     bitmap whose word is t & 4095) or general layout (scattered bitmap).
 //
 // A chunk's Max-IDF score ln(N / mindf) is strictly decreasing in mindf, so
 // ranking by (mindf ascending, index ascending) is ranking by (score
@@ -54,36 +64,55 @@ constexpr int kFastWords = 1 << kFastWordsLog2;
 constexpr int kFastBitmapBytes = kFastWords * 4;
 constexpr int kFastVocab = kFastWords * 32;
 // Register-resident variant (see maxidf_resident_kernel): rounds of 2 groups
-// of 4 ids per thread, at most RES_ROUNDS of them per sequence.
+// of 4 ids per thread, a power of two up to RES_ROUNDS of them per sequence.
+// Its static LDS holds the stamp-code table (vocab <= 131072 bytes) and,
+// behind it, the chunk minima (at most kResChunkBytes).
 constexpr int RES_ROUNDS = 16;
 constexpr int RES_ROUND_TOKENS = MAXIDF_THREADS * 8;
-// The resident variant alternates two compact bitmaps (block j marks bitmap
-// j % 2 and clears the other), so its df bytes start at byte 32768.
-constexpr int kResBitmapBytes = 2 * kFastBitmapBytes;
+constexpr int kResChunkBytes = PULSAR_LDS_BYTES - kFastVocab;
+
+// Stamp code: one byte per id, 16 * (15 - j) + (df - 1) after the id was
+// last seen in block j with df blocks so far (1 <= df <= j + 1 <= 16), or
+// kStampNever before it is first seen.  Once pass 1 is over the low nibble of
+// every seen id is df - 1 (stamp_to_df).
+constexpr int kStampMaxBlocks = 16;
+// word 3 of a buffer resource for raw 32-bit-offset access
+constexpr int kRawBuffer = 0x00020000;
+constexpr uint32_t kStampNever = 0xFFu;
+
+enum MaxidfMode { kGeneral = 0, kCompact = 1, kStamp = 2 };
 
 struct MaxidfPlan {
-  bool fast;
-  bool resident;     // compact layout with the ids held in registers
+  int mode;          // MaxidfMode of the streaming kernel
+  bool resident;     // stamp code with the ids held in registers
   int64_t lds_bytes;
   int64_t cmin_off;  // byte offset of the chunk minima
 };
 
-// General layout: df bytes [round_up4(vocab)], then a region reused as the
-// per-block bitmap (pass 1) and the chunk minima (pass 2 / select).
+// Streaming layouts: the df (or stamp-code) bytes [round_up4(vocab)] at LDS
+// byte 0 (general, stamp) or 16384 (compact); the general layout reuses the
+// region behind the table as the per-block bitmap (pass 1) and the chunk
+// minima (pass 2 / select).
 static MaxidfPlan maxidf_plan(int64_t L, int num_blocks, int chunk, int vocab) {
   const int64_t df_bytes = round_up4(vocab);
   const int64_t chunk_bytes = round_up4(L / chunk);
+  // L = 8192 * (a power of two up to 16), blocks of a multiple of 8192 ids
+  // (so N <= 16 and the rounds per block are a power of two)
+  const int64_t res_rounds = L / RES_ROUND_TOKENS;
+  if (vocab <= kFastVocab && L % RES_ROUND_TOKENS == 0 && res_rounds <= RES_ROUNDS &&
+      (res_rounds & (res_rounds - 1)) == 0 && (L / num_blocks) % RES_ROUND_TOKENS == 0 &&
+      chunk_bytes <= kResChunkBytes)
+    return {kStamp, true, PULSAR_LDS_BYTES, kFastVocab};
+  if (num_blocks <= kStampMaxBlocks && df_bytes + chunk_bytes <= PULSAR_LDS_BYTES)
+    return {kStamp, false, df_bytes + chunk_bytes, df_bytes};
   if (vocab <= kFastVocab) {
-    if (L <= (int64_t)RES_ROUNDS * RES_ROUND_TOKENS && (L / num_blocks) % RES_ROUND_TOKENS == 0 &&
-        chunk_bytes <= kResBitmapBytes)  // static LDS: bitmaps + the largest df table
-      return {true, true, kResBitmapBytes + kFastVocab, 0};
     const bool in_bitmap = chunk_bytes <= kFastBitmapBytes;
     const int64_t lds = kFastBitmapBytes + df_bytes + (in_bitmap ? 0 : chunk_bytes);
     if (lds <= PULSAR_LDS_BYTES)
-      return {true, false, lds, in_bitmap ? 0 : kFastBitmapBytes + df_bytes};
+      return {kCompact, false, lds, in_bitmap ? 0 : kFastBitmapBytes + df_bytes};
   }
   const int64_t bitmap_bytes = bitmap_words(vocab) * 4;
-  return {false, false, df_bytes + (bitmap_bytes > chunk_bytes ? bitmap_bytes : chunk_bytes),
+  return {kGeneral, false, df_bytes + (bitmap_bytes > chunk_bytes ? bitmap_bytes : chunk_bytes),
           df_bytes};
 }
 
@@ -140,28 +169,87 @@ __device__ __forceinline__ void mark_tokens_compact(const int (&t)[n], uint32_t 
     if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] << 3) & 31));
 }
 
+// Stamp code, block j: an id whose byte is not yet stamped with j gets the
+// code of (df + 1, j).  With base = 16 * (15 - j), the codes stamped with j
+// are base .. base + j (df - 1 <= j); the code of an id last seen in an
+// earlier block, and kStampNever, lie above that range, and their low nibble
+// plus one (mod 16) is the new df - 1.  All lanes that write one byte during
+// block j write the same value, whatever order their loads and stores take,
+// so the count is exact without atomics as long as no two blocks run at once
+// (the caller puts a workgroup barrier between blocks).  PAD: the round holds
+// -1 padding, which stamps nothing.  An id at or above vocab is clamped into
+// the table (the caller's error).
+template <int n, bool PAD>
+__device__ __forceinline__ void stamp_tokens(const int (&t)[n], int j, uint32_t vmax,
+                                             uint8_t* code) {
+  uint32_t ts[n], c[n];
+#pragma unroll
+  for (int i = 0; i < n; ++i) ts[i] = min((uint32_t)t[i], vmax);
+#pragma unroll
+  for (int i = 0; i < n; ++i) c[i] = code[ts[i]];
+  const uint32_t base = 16u * (15u - (uint32_t)j);
+#pragma unroll
+  for (int i = 0; i < n; ++i) {
+    const bool stamped = c[i] - base <= (uint32_t)j;
+    if (!stamped && (!PAD || t[i] >= 0)) code[ts[i]] = (uint8_t)(base | ((c[i] + 1u) & 15u));
+  }
+}
+
+// After pass 1: every stamp code becomes df - 1 (its low nibble), four ids
+// per word.  Only ids never seen (kStampNever) read as df 16; no id of the
+// sequence is one of them.
+__device__ __forceinline__ void stamp_to_df(uint32_t* codew, int vocab_w4, int tid) {
+  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) codew[w] &= 0x0F0F0F0Fu;
+}
+
+// df of a stamp code after pass 1 (0 for an id never seen)
+__device__ __forceinline__ uint32_t stamp_df(uint32_t c) {
+  return c == kStampNever ? 0u : (c & 15u) + 1u;
+}
+
 __device__ __forceinline__ uint32_t df_of(int t, int vocab, const uint8_t* df8) {
   return df8[min((uint32_t)t, (uint32_t)(vocab - 1))];
+}
+
+// x moved across lanes by a DPP control (quad permutes, row mirrors)
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+// Minimum over aligned groups of 2^GL lanes, the group size a compile-time
+// constant; every lane of a group ends with the group's minimum.
+template <int GL>
+__device__ __forceinline__ uint32_t group_min_c(uint32_t x) {
+  if (GL >= 1) x = min(x, dpp_mov<0xB1>(x));   // lane ^ 1
+  if (GL >= 2) x = min(x, dpp_mov<0x4E>(x));   // lane ^ 2
+  if (GL >= 3) x = min(x, dpp_mov<0x141>(x));  // mirror within 8
+  if (GL >= 4) x = min(x, dpp_mov<0x140>(x));  // mirror within 16
+  if (GL >= 5) x = min(x, (uint32_t)__shfl_xor((int)x, 16, 64));
+  if (GL >= 6) x = min(x, (uint32_t)__shfl_xor((int)x, 32, 64));
+  return x;
 }
 
 // Minimum over aligned groups of `group` lanes (a power of two); DPP within
 // rows of 16 lanes, cross-lane permutes beyond.
 __device__ __forceinline__ uint32_t group_min(uint32_t x, int group) {
-  if (group >= 2) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0xB1, 0xF, 0xF, false));
-  if (group >= 4) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x4E, 0xF, 0xF, false));
-  if (group >= 8) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x141, 0xF, 0xF, false));
-  if (group >= 16) x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x140, 0xF, 0xF, false));
+  if (group >= 2) x = min(x, dpp_mov<0xB1>(x));
+  if (group >= 4) x = min(x, dpp_mov<0x4E>(x));
+  if (group >= 8) x = min(x, dpp_mov<0x141>(x));
+  if (group >= 16) x = min(x, dpp_mov<0x140>(x));
   if (group >= 32) x = min(x, (uint32_t)__shfl_xor((int)x, 16, 64));
   if (group >= 64) x = min(x, (uint32_t)__shfl_xor((int)x, 32, 64));
   return x;
 }
 
-// Optional IDF table (Eq. idf) of one sequence from its df bytes in LDS.
+// Optional IDF table (Eq. idf) of one sequence from its df bytes (STAMP:
+// stamp codes) in LDS.
+template <bool STAMP>
 __device__ void write_idf(const uint8_t* df8, int vocab, int num_blocks, float* __restrict__ out,
                           int tid) {
   const float n = (float)num_blocks;
   for (int t = tid; t < vocab; t += MAXIDF_THREADS) {
-    const uint32_t d = df8[t];
+    const uint32_t d = STAMP ? stamp_df(df8[t]) : df8[t];
     out[t] = logf(n / (float)(d > 1u ? d : 1u));
   }
 }
@@ -171,47 +259,72 @@ __device__ __forceinline__ int count_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
 }
 
-// Top-k chunks of every block of sequence b from the chunk minima cmin
-// ([num_blocks][C] bytes in LDS), written in ascending chunk order.  One
-// wavefront per block; slot i of lane l is chunk 64*i + l, so chunk order is
-// (slot, lane) order and every count is a ballot.  The threshold tau is the
-// smallest df with at least k chunks at or below it (binary search over
-// 1..N); every chunk below tau is kept, and the first k - #(< tau) chunks
-// equal to tau in chunk order.
-__device__ void select_topk(const uint8_t* cmin, int64_t b, int num_blocks, int C, int topk,
-                            int32_t* __restrict__ sel, int wave, int lane) {
-  if (topk == 0) return;
+// Top-k chunks of one block from its chunk minima cv ([C] bytes in LDS),
+// written in ascending chunk order to dst.  Slot i of lane l is chunk
+// 64*i + l, so chunk order is (slot, lane) order and every count is a ballot.
+// The threshold tau is the smallest df with at least k chunks at or below it
+// (binary search over 1..N); every chunk below tau is kept, and the first
+// k - #(< tau) chunks equal to tau in chunk order.  S > 0: the block has at
+// most S slots and their values are held in registers; S == 0: any number of
+// slots, read from LDS each time.
+template <int S>
+__device__ __forceinline__ void select_block(const uint8_t* cv, int C, int num_blocks, int topk,
+                             int32_t* __restrict__ dst, int lane) {
   const int slots = (C + 63) >> 6;
-  for (int j = wave; j < num_blocks; j += MAXIDF_WAVES) {
+  const int n_slots = S > 0 ? S : slots;
+  constexpr int R = S > 0 ? S : 1;
+  int xr[R];
+  // a lane past the last chunk holds 256, above every df (<= 255)
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+    xr[i] = (S > 0 && i < slots && 64 * i + lane < C) ? (int)cv[64 * i + lane] : 256;
+#define SEL_X(i) \
+  (S > 0 ? xr[S > 0 ? (i) : 0] : (64 * (i) + lane < C ? (int)cv[64 * (i) + lane] : 256))
+  int lo = 0, hi = num_blocks;  // #(mindf <= lo) < k <= #(mindf <= hi)
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < n_slots; ++i) cnt += __popcll(__ballot(SEL_X(i) <= mid));
+    if (cnt >= topk) hi = mid; else lo = mid;
+  }
+  const int tau = hi;
+  int n_lt = 0;
+#pragma unroll
+  for (int i = 0; i < n_slots; ++i) n_lt += __popcll(__ballot(SEL_X(i) < tau));
+  const int need = topk - n_lt;  // kept chunks equal to tau
+  int eq_before = 0, out_before = 0;
+#pragma unroll
+  for (int i = 0; i < n_slots; ++i) {
+    const int x = SEL_X(i);
+    const uint64_t m_eq = __ballot(x == tau);
+    const bool keep = x < tau || (x == tau && eq_before + count_below(m_eq) < need);
+    const uint64_t m_keep = __ballot(keep);
+    if (keep) dst[out_before + count_below(m_keep)] = 64 * i + lane;
+    eq_before += __popcll(m_eq);
+    out_before += __popcll(m_keep);
+  }
+#undef SEL_X
+}
+
+// Top-k chunks of every block of sequence b from the chunk minima cmin
+// ([num_blocks][C] bytes in LDS); one wavefront per block.
+__device__ __forceinline__ void select_topk(const uint8_t* cmin, int64_t b, int num_blocks, int C,
+                                            int topk, int32_t* __restrict__ sel, int wave,
+                                            int lane) {
+  if (topk == 0) return;
+  // the block loop is uniform across the wavefront: keep it scalar
+  for (int j = __builtin_amdgcn_readfirstlane(wave); j < num_blocks; j += MAXIDF_WAVES) {
     const uint8_t* cv = cmin + (int64_t)j * C;
-    // a lane past the last chunk reads 256, above every df (<= 255)
-    auto x_of = [&](int i) { return 64 * i + lane < C ? (int)cv[64 * i + lane] : 256; };
-    int lo = 0, hi = num_blocks;  // #(mindf <= lo) < k <= #(mindf <= hi)
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      int cnt = 0;
-      for (int i = 0; i < slots; ++i) cnt += __popcll(__ballot(x_of(i) <= mid));
-      if (cnt >= topk) hi = mid; else lo = mid;
-    }
-    const int tau = hi;
-    int n_lt = 0;
-    for (int i = 0; i < slots; ++i) n_lt += __popcll(__ballot(x_of(i) < tau));
-    const int need = topk - n_lt;  // chunks equal to tau that are kept
     int32_t* dst = sel + (b * num_blocks + j) * topk;
-    int eq_before = 0, out_before = 0;
-    for (int i = 0; i < slots; ++i) {
-      const int x = x_of(i);
-      const uint64_t m_eq = __ballot(x == tau);
-      const bool keep = x < tau || (x == tau && eq_before + count_below(m_eq) < need);
-      const uint64_t m_keep = __ballot(keep);
-      if (keep) dst[out_before + count_below(m_keep)] = 64 * i + lane;
-      eq_before += __popcll(m_eq);
-      out_before += __popcll(m_keep);
-    }
+    if (C <= 4 * 64)
+      select_block<4>(cv, C, num_blocks, topk, dst, lane);
+    else
+      select_block<0>(cv, C, num_blocks, topk, dst, lane);
   }
 }
 
-template <bool COMPACT>
+template <int MODE>
 __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
     const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2,
     int topk, int vocab, int n_bitmap, int spread_mask, int cmin_off, int32_t* __restrict__ sel,
@@ -224,7 +337,9 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   const int chunk = 1 << chunk_log2;
   const int vocab_w4 = (vocab + 3) >> 2;
   uint8_t* const lds8 = reinterpret_cast<uint8_t*>(lds);
-  uint8_t* df8 = lds8 + (COMPACT ? kFastBitmapBytes : 0);
+  constexpr bool COMPACT = MODE == kCompact;
+  constexpr bool STAMP = MODE == kStamp;
+  uint8_t* df8 = lds8 + (COMPACT ? kFastBitmapBytes : 0);  // df bytes or stamp codes
   uint32_t* dfw = reinterpret_cast<uint32_t*>(df8);
   uint32_t* bits = COMPACT ? lds : lds + vocab_w4;
   uint8_t* cmin = lds8 + cmin_off;
@@ -232,8 +347,9 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
 
   const int32_t* seq = ids + b * L;
 
-  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = 0u;
-  // (the first round's barrier orders this against the atomics)
+  const uint32_t init = STAMP ? kStampNever * 0x01010101u : 0u;
+  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = init;
+  // (the first round's barrier orders this against pass 1)
 
   // ---- pass 1: document frequency --------------------------------------
   // The blocks are streamed as rounds of MAXIDF_THREADS x ROUND int4 groups;
@@ -265,10 +381,12 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   for (int i = 0; i < PREFETCH; ++i)
     if (i < rounds) load_round(i, cbuf[i]);
   for (int rd = 0; rd < rounds; ++rd) {
-    if (rd % rpb == 0) {  // a new block: everyone is done with the previous bitmap
+    if (rd % rpb == 0) {  // a new block: everyone is done with the previous one
       __syncthreads();
-      for (int w = tid; w < n_bitmap; w += MAXIDF_THREADS) bits[w] = 0u;
-      __syncthreads();
+      if constexpr (!STAMP) {
+        for (int w = tid; w < n_bitmap; w += MAXIDF_THREADS) bits[w] = 0u;
+        __syncthreads();
+      }
     }
     if (rd + PREFETCH < rounds) load_round(rd + PREFETCH, cbuf[PREFETCH]);
     {
@@ -280,8 +398,14 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
         tk[4 * u + 2] = cbuf[0][u].z;
         tk[4 * u + 3] = cbuf[0][u].w;
       }
-      if constexpr (COMPACT) {
-        if ((rd - (rd / rpb) * rpb + 1) * ROUND * MAXIDF_THREADS <= nvec)
+      const bool full = (rd - (rd / rpb) * rpb + 1) * ROUND * MAXIDF_THREADS <= nvec;
+      if constexpr (STAMP) {
+        if (full)
+          stamp_tokens<4 * ROUND, false>(tk, rd / rpb, vmax, df8);
+        else
+          stamp_tokens<4 * ROUND, true>(tk, rd / rpb, vmax, df8);
+      } else if constexpr (COMPACT) {
+        if (full)
           mark_tokens_compact<4 * ROUND, false>(tk, vmax, bits, dfw);
         else
           mark_tokens_compact<4 * ROUND, true>(tk, vmax, bits, dfw);
@@ -297,9 +421,15 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   }
   __syncthreads();
 
-  if (idf) write_idf(df8, vocab, num_blocks, idf + b * vocab, tid);
+  if (idf) write_idf<STAMP>(df8, vocab, num_blocks, idf + b * vocab, tid);
+  if constexpr (STAMP) {
+    if (idf) __syncthreads();
+    stamp_to_df(dfw, vocab_w4, tid);
+    __syncthreads();
+  }
 
   // ---- pass 2: per-chunk minimum df -------------------------------------
+  // (STAMP: the table holds df - 1)
   // Groups of PF int4 loads per thread, double-buffered: group g+1 is in
   // flight while group g is reduced.  Every lane runs the same trip count,
   // so all lanes join the cross-lane minimum.
@@ -329,6 +459,7 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
       uint32_t mn = min(min(df_of(t[p].x, vocab, df8), df_of(t[p].y, vocab, df8)),
                         min(df_of(t[p].z, vocab, df8), df_of(t[p].w, vocab, df8)));
       mn = group_min(mn, group);
+      if (STAMP) mn += 1u;
       if ((lane & (group - 1)) == 0 && v < nvec_seq) {
         const int c = v >> group_log2;
         cmin[c] = (uint8_t)mn;
@@ -350,116 +481,192 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   select_topk(cmin, b, num_blocks, Lb >> chunk_log2, topk, sel, wave, lane);
 }
 
-// Register-resident variant for the compact layout when the sequence fits
-// the register file: L <= 131072 and Lb a multiple of 8192, so that every
-// thread owns exactly RES_ROUNDS x 2 16-byte groups of ids.  Pass 1 keeps
-// each thread's ids in registers (the clamped id's low 16 bits packed two per
-// register, bit 16 of all of them in four more registers), and pass 2 reads
-// them back from there: the ids cross HBM once.  Thread tid's group u of
-// round rd is the sequence's 16-byte group (2*rd + u)*1024 + tid, which is
-// also the group pass 2 assigns to iteration 2*rd + u.
+// Register-resident variant with the stamp code when the sequence fits the
+// register file: L = ROUNDS * 8192 with ROUNDS a power of two up to 16, and
+// Lb a multiple of 8192, so that every thread owns exactly ROUNDS x 2
+// 16-byte groups of ids.  Pass 1 keeps each thread's ids in registers and
+// pass 2 reads them back from there: the ids cross HBM once.  Thread tid's
+// group u of round rd is the sequence's 16-byte group (2*rd + u)*1024 + tid,
+// which is also the group pass 2 assigns to slot 2*rd + u.
+//
+// Packing of the 4 clamped ids (< 2^17) of slot s: their low 16 bits two per
+// register (plo), and their bit 16 in byte i of hb[s / 8] at bit s % 8 --
+// each made and undone by byte permutes.
+//
+// Persistent: workgroup g takes sequences g, g + G, ... (G = gridDim.x, one
+// workgroup per compute unit).  With CARRY_NEXT (more sequences than
+// workgroups), pass 2 of one sequence frees the packed ids two rounds at a
+// time and the first CARRY rounds of the next sequence are loaded into the
+// freed registers, so HBM keeps streaming while the compute unit is busy
+// with pass 2 and the top-k select.  Past the last sequence the next
+// sequence's buffer resource covers no bytes, and those loads return zeros
+// without touching memory.
+//
+// ROUNDS and the chunk's lane group (GL = log2(chunk / 4), or -1 for any)
+// are template arguments, so that the loops are straight-line code: every
+// load's wait is exact and the cross-lane minimum has no branches.
+template <int ROUNDS, int GL, bool CARRY_NEXT>
 __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
-    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2,
+    const int32_t* __restrict__ ids, int batch, int num_blocks, int rpb_log2, int chunk_log2,
     int topk, int vocab, int32_t* __restrict__ sel, int32_t* __restrict__ chunk_mindf,
     float* __restrict__ idf) {
   // A fixed layout in static LDS, whose base the compiler knows, so every
-  // table offset folds into the LDS instructions: two bitmaps, then the df
-  // bytes (vocab <= 131072); the chunk minima (<= 32 KiB) reuse the bitmaps.
-  __shared__ __attribute__((aligned(16))) uint32_t lds[(kResBitmapBytes + kFastVocab) / 4];
+  // table offset folds into the LDS instructions: the stamp codes (vocab <=
+  // 131072 bytes), then the chunk minima (<= kResChunkBytes).
+  __shared__ __attribute__((aligned(16))) uint32_t lds[PULSAR_LDS_BYTES / 4];
+  constexpr int64_t L = (int64_t)ROUNDS * RES_ROUND_TOKENS;
+  // rounds of the next sequence loaded during pass 2
+  constexpr int CARRY = CARRY_NEXT ? ROUNDS / 2 : 0;
+  constexpr int PREFETCH = 2;        // rounds of loads in flight during pass 1
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int64_t b = blockIdx.x;
   uint8_t* const lds8 = reinterpret_cast<uint8_t*>(lds);
-  uint8_t* df8 = lds8 + kResBitmapBytes;
-  uint32_t* dfw = reinterpret_cast<uint32_t*>(df8);
-  uint8_t* cmin = lds8;
+  uint8_t* code8 = lds8;
+  uint32_t* codew = lds;
+  uint8_t* cmin = lds8 + kFastVocab;
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const int vocab_w4 = (vocab + 3) >> 2;
-  const int4* seq4 = reinterpret_cast<const int4*>(ids + b * L);
-  const int rounds = (int)(L / RES_ROUND_TOKENS);  // <= RES_ROUNDS
-  const int rpb = Lb / RES_ROUND_TOKENS;            // rounds per block
+  const uint32_t lane_off = (uint32_t)tid * 16u;
+  const int group_log2 = GL >= 0 ? GL : chunk_log2 - 2;  // lanes per chunk: 1..64
+  const int group = 1 << group_log2;
+  const int nchunks_seq = (int)(L >> (group_log2 + 2));
 
-  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) dfw[w] = 0u;
-  for (int w = tid; w < 2 * kFastWords; w += MAXIDF_THREADS) lds[w] = 0u;
-  __syncthreads();
-
-  // ---- pass 1: document frequency, ids kept in registers ------------------
-  constexpr int PREFETCH = 2;  // rounds of loads in flight
-  int4 cbuf[PREFETCH + 1][2];
-  uint32_t plo[RES_ROUNDS][2][2];         // low 16 bits, two ids per register
-  uint32_t phi[RES_ROUNDS * 2 / 8] = {};  // bit 16 of every id, 32 per register
-  auto load_round = [&](int rd, int4 (&t)[2]) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) t[u] = seq4[(2 * rd + u) * MAXIDF_THREADS + tid];
+  // a sequence's ids through a buffer resource (no bytes past the batch):
+  // one lane offset, and each group's offset a scalar constant
+  auto seq_rsrc = [&](int64_t b) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(ids + (b < batch ? b : 0) * L),
+                                             (short)0, b < batch ? (int)(L * 4) : 0, kRawBuffer);
   };
+  auto load_round = [&](__amdgpu_buffer_rsrc_t r, int rd, int4 (&t)[2]) {
 #pragma unroll
-  for (int i = 0; i < PREFETCH; ++i)
-    if (i < rounds) load_round(i, cbuf[i]);
+    for (int u = 0; u < 2; ++u) {
+      const auto v =
+          __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, (2 * rd + u) * MAXIDF_THREADS * 16, 0);
+      t[u] = make_int4((int)v[0], (int)v[1], (int)v[2], (int)v[3]);
+    }
+  };
+
+  int4 nbuf[CARRY > 0 ? CARRY : 1][2];  // the next sequence's first CARRY rounds
+  {
+    const __amdgpu_buffer_rsrc_t r0 = seq_rsrc(blockIdx.x);
 #pragma unroll
-  for (int rd = 0; rd < RES_ROUNDS; ++rd) {
-    if (rd < rounds) {
-      // Block j marks bitmap j % 2.  At its start every wave is past block
-      // j-1 (barrier), so the other bitmap is cleared for block j+1 while
-      // this one is marked.
-      const int j = rd / rpb;
-      uint32_t* bits = lds + (j & 1) * kFastWords;
-      if (rd % rpb == 0) {
-        if (rd > 0) __syncthreads();
-        uint32_t* other = lds + ((j + 1) & 1) * kFastWords;
-        for (int w = tid; w < kFastWords; w += MAXIDF_THREADS) other[w] = 0u;
-      }
-      if (rd + PREFETCH < rounds)
-        load_round(rd + PREFETCH, cbuf[(rd + PREFETCH) % (PREFETCH + 1)]);
-      const int4 (&cur)[2] = cbuf[rd % (PREFETCH + 1)];
-      int tk[8];
+    for (int rd = 0; rd < CARRY; ++rd) load_round(r0, rd, nbuf[rd]);
+  }
+
+  for (int64_t b = blockIdx.x; b < batch; b += gridDim.x) {
+    const __amdgpu_buffer_rsrc_t rsrc = seq_rsrc(b);
+    const __amdgpu_buffer_rsrc_t rnext = seq_rsrc(b + gridDim.x);
+
+    // ---- pass 1: document frequency, ids kept in registers ----------------
+    int4 cbuf[PREFETCH + 1][2];
+    uint32_t plo[ROUNDS][2][2];              // low 16 bits, two ids per register
+    uint32_t hb[(ROUNDS * 2 + 7) / 8] = {};  // bit 16 of the ids of slot s: bit s % 8 of each byte
+    // the first loads are in flight while the table is cleared
+#pragma unroll
+    for (int i = CARRY; i < CARRY + PREFETCH && i < ROUNDS; ++i)
+      load_round(rsrc, i, cbuf[i % (PREFETCH + 1)]);
+    {
+      const uint4 never = make_uint4(kStampNever * 0x01010101u, kStampNever * 0x01010101u,
+                                     kStampNever * 0x01010101u, kStampNever * 0x01010101u);
+      uint4* code16 = reinterpret_cast<uint4*>(lds);
+      for (int w = tid; w < (vocab_w4 + 3) >> 2; w += MAXIDF_THREADS) code16[w] = never;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rd = 0; rd < ROUNDS; ++rd) {
+      // block j starts once every wave is past block j - 1
+      const int j = rd >> rpb_log2;
+      if (rd > 0 && (rd & ((1 << rpb_log2) - 1)) == 0) __syncthreads();
+      if (rd >= CARRY && rd + PREFETCH < ROUNDS)
+        load_round(rsrc, rd + PREFETCH, cbuf[(rd + PREFETCH) % (PREFETCH + 1)]);
+      const int4 (&cur)[2] = rd < CARRY ? nbuf[rd < CARRY ? rd : 0] : cbuf[rd % (PREFETCH + 1)];
+      // one 16-byte group at a time (measured faster than all 8 ids of the
+      // round together)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int4 x = cur[u];
         const uint32_t t0 = min((uint32_t)x.x, vmax), t1 = min((uint32_t)x.y, vmax);
         const uint32_t t2 = min((uint32_t)x.z, vmax), t3 = min((uint32_t)x.w, vmax);
-        tk[4 * u] = (int)t0;
-        tk[4 * u + 1] = (int)t1;
-        tk[4 * u + 2] = (int)t2;
-        tk[4 * u + 3] = (int)t3;
+        const int tk[4] = {(int)t0, (int)t1, (int)t2, (int)t3};
+        const int slot = 2 * rd + u;
         plo[rd][u][0] = __builtin_amdgcn_perm(t1, t0, 0x05040100u);
         plo[rd][u][1] = __builtin_amdgcn_perm(t3, t2, 0x05040100u);
-        const uint32_t h =
-            ((t0 >> 16) & 1u) | ((t1 >> 15) & 2u) | ((t2 >> 14) & 4u) | ((t3 >> 13) & 8u);
-        const int slot = 2 * rd + u;
-        phi[slot >> 3] |= h << (4 * (slot & 7));
+        // byte i of h4 = bit 16 of id i
+        const uint32_t h4 = __builtin_amdgcn_perm(t1, t0, 0x0C0C0602u) |
+                            (__builtin_amdgcn_perm(t3, t2, 0x0C0C0602u) << 16);
+        hb[slot >> 3] |= h4 << (slot & 7);
+        // packed here, not next to pass 2: the compiler would otherwise keep
+        // the unpacked ids alive
+        asm volatile("" : "+v"(plo[rd][u][0]), "+v"(plo[rd][u][1]), "+v"(hb[slot >> 3]));
+        stamp_tokens<4, false>(tk, j, vmax, code8);
       }
-      mark_tokens_compact<8, false>(tk, vmax, bits, dfw);
     }
-  }
-  __syncthreads();
-  if (idf) write_idf(df8, vocab, num_blocks, idf + b * vocab, tid);
+    __syncthreads();
+    if (idf) {
+      write_idf<true>(code8, vocab, num_blocks, idf + b * vocab, tid);
+      __syncthreads();
+    }
+    stamp_to_df(codew, vocab_w4, tid);
+    __syncthreads();
 
-  // ---- pass 2: per-chunk minimum df from the registers --------------------
-  const int group = 1 << (chunk_log2 - 2);  // lanes per chunk (1..64)
-  const int group_log2 = chunk_log2 - 2;
-  const int nchunks_seq = (int)(L >> chunk_log2);
+    // ---- pass 2: per-chunk minimum df from the registers ------------------
+    // (the thread index is re-formed in every iteration: values derived from
+    // it would otherwise be hoisted out of the sequence loop and held in
+    // registers throughout)
+    int tid_i = tid;
+    asm volatile("" : "+v"(tid_i));
 #pragma unroll
-  for (int slot = 0; slot < 2 * RES_ROUNDS; ++slot) {
-    if (slot < 2 * rounds) {
+    for (int slot = 0; slot < 2 * ROUNDS; ++slot) {
       const uint32_t lo0 = plo[slot >> 1][slot & 1][0], lo1 = plo[slot >> 1][slot & 1][1];
-      const uint32_t h = phi[slot >> 3] >> (4 * (slot & 7));
-      const uint32_t t0 = (lo0 & 0xFFFFu) | ((h & 1u) << 16);
-      const uint32_t t1 = (lo0 >> 16) | ((h & 2u) << 15);
-      const uint32_t t2 = (lo1 & 0xFFFFu) | ((h & 4u) << 14);
-      const uint32_t t3 = (lo1 >> 16) | ((h & 8u) << 13);
-      uint32_t mn = min(min((uint32_t)df8[t0], (uint32_t)df8[t1]),
-                        min((uint32_t)df8[t2], (uint32_t)df8[t3]));
-      mn = group_min(mn, group);
-      if ((lane & (group - 1)) == 0) {
-        const int c = (slot * MAXIDF_THREADS + tid) >> group_log2;
+      const uint32_t x = (hb[slot >> 3] >> (slot & 7)) & 0x01010101u;
+      const uint32_t t0 = __builtin_amdgcn_perm(x, lo0, 0x0C040100u);
+      const uint32_t t1 = __builtin_amdgcn_perm(x, lo0, 0x0C050302u);
+      const uint32_t t2 = __builtin_amdgcn_perm(x, lo1, 0x0C060100u);
+      const uint32_t t3 = __builtin_amdgcn_perm(x, lo1, 0x0C070302u);
+      // the table holds df - 1
+      uint32_t mn = min(min((uint32_t)code8[t0], (uint32_t)code8[t1]),
+                        min((uint32_t)code8[t2], (uint32_t)code8[t3]));
+      if constexpr (GL >= 0) mn = group_min_c<GL>(mn);
+      else mn = group_min(mn, group);
+      mn += 1u;
+      if ((tid_i & (group - 1)) == 0) {
+        const int c = (slot * MAXIDF_THREADS + tid_i) >> group_log2;
         cmin[c] = (uint8_t)mn;
         if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
       }
+      // every fourth slot frees two rounds of packed ids: load one round of
+      // the next sequence in their place
+      if ((slot & 3) == 3 && (slot >> 2) < CARRY) {
+        __builtin_amdgcn_sched_barrier(0);
+        load_round(rnext, slot >> 2, nbuf[(slot >> 2) < CARRY ? (slot >> 2) : 0]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+    __syncthreads();
+    select_topk(cmin, b, num_blocks, (int)(L / num_blocks) >> chunk_log2, topk, sel, wave, lane);
   }
-  __syncthreads();
-  select_topk(cmin, b, num_blocks, Lb >> chunk_log2, topk, sel, wave, lane);
+}
+
+// Resident kernels by (rounds, chunk): the lane group is a template argument
+// for chunks of 16 and 32 ids, the common sizes.
+typedef void (*ResidentKernel)(const int32_t*, int, int, int, int, int, int, int32_t*, int32_t*,
+                               float*);
+template <int ROUNDS, bool CARRY_NEXT>
+static ResidentKernel resident_for_chunk(int chunk_log2) {
+  if (chunk_log2 == 5) return maxidf_resident_kernel<ROUNDS, 3, CARRY_NEXT>;
+  if (chunk_log2 == 4) return maxidf_resident_kernel<ROUNDS, 2, CARRY_NEXT>;
+  return maxidf_resident_kernel<ROUNDS, -1, CARRY_NEXT>;
+}
+template <bool CARRY_NEXT>
+static ResidentKernel resident_kernel(int rounds, int chunk_log2) {
+  switch (rounds) {
+    case 16: return resident_for_chunk<16, CARRY_NEXT>(chunk_log2);
+    case 8: return resident_for_chunk<8, CARRY_NEXT>(chunk_log2);
+    case 4: return resident_for_chunk<4, CARRY_NEXT>(chunk_log2);
+    case 2: return resident_for_chunk<2, CARRY_NEXT>(chunk_log2);
+    default: return resident_for_chunk<1, CARRY_NEXT>(chunk_log2);
+  }
 }
 
 int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
@@ -471,16 +678,31 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
   const MaxidfPlan plan = maxidf_plan(L, num_blocks, chunk, vocab);
   if ((size_t)plan.lds_bytes != lds_bytes) return PULSAR_EINVAL;
   if (plan.resident) {  // static LDS only
-    hipLaunchKernelGGL(maxidf_resident_kernel, dim3(batch), dim3(MAXIDF_THREADS), 0, stream, ids,
-                       L, num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, sel,
-                       chunk_mindf, idf);
+    const int rounds = (int)(L / RES_ROUND_TOKENS);
+    int rpb_log2 = 0;
+    while ((RES_ROUND_TOKENS << rpb_log2) < L / num_blocks) ++rpb_log2;
+    // one workgroup per compute unit (160 KB of LDS each), persistent over
+    // the batch; the next sequence's ids are carried only when a workgroup
+    // has more than one sequence
+    int dev = 0, n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n_cu < 1)
+      return PULSAR_EHIP;
+    const int grid = batch < n_cu ? batch : n_cu;
+    const ResidentKernel kern = batch > grid ? resident_kernel<true>(rounds, chunk_log2)
+                                             : resident_kernel<false>(rounds, chunk_log2);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(MAXIDF_THREADS), 0, stream, ids, batch, num_blocks,
+                       rpb_log2, chunk_log2, topk, vocab, sel, chunk_mindf, idf);
     return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
   }
-  const auto kern = plan.fast ? maxidf_kernel<true> : maxidf_kernel<false>;
+  const auto kern = plan.mode == kStamp     ? maxidf_kernel<kStamp>
+                    : plan.mode == kCompact ? maxidf_kernel<kCompact>
+                                            : maxidf_kernel<kGeneral>;
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds_bytes) != hipSuccess)
     return PULSAR_EHIP;
-  const int64_t nb = plan.fast ? kFastWords : bitmap_words(vocab);
+  const int64_t nb = plan.mode == kCompact ? kFastWords : bitmap_words(vocab);
   const bool pow2 = (nb & (nb - 1)) == 0;
   hipLaunchKernelGGL(kern, dim3(batch), dim3(MAXIDF_THREADS), lds_bytes, stream, ids, L,
                      num_blocks, (int)(L / num_blocks), chunk_log2, topk, vocab, (int)nb,

@@ -130,3 +130,21 @@ def test_positions_ragged_shapes():
         pos = P.phase1_positions(sel, 1, L, N, i, s, m, k).cpu().numpy()[0]
         assert np.array_equal(pos, assembly.phase1_positions(L, N, i, s, m, k, sel_ref[0]))
     assert math.isfinite(float(pos.sum()))
+
+
+@pytest.mark.parametrize("L,N,batch,m", [(131072, 16, 600, 32), (16384, 2, 700, 16),
+                                         (65536, 8, 520, 64)])
+def test_batch_beyond_compute_units(L, N, batch, m):
+    # More sequences than compute units: each workgroup runs several of them
+    # in turn and loads the next one's first ids while finishing the current
+    # one.  Three distinct sequences repeat through the batch, so the oracle
+    # runs three times and every output row is checked.
+    base = np.stack([workload.zipf_ids(4000 + L // 1024 + i, L, 128256) for i in range(3)])
+    print(f"maxidf persistent: batch={batch} L={L} N={N} m={m}", flush=True)
+    sel_ref, mindf_ref, _, _ = maxidf.maxidf_summaries(base, N, m, 7, 128256)
+    ids = base[np.arange(batch) % 3]
+    sel, mindf = P.maxidf_summaries(to_dev_i32(ids), N, m, 7, 128256, return_mindf=True)
+    sel, mindf = sel.cpu().numpy(), mindf.cpu().numpy()
+    for r in range(3):
+        assert np.array_equal(sel[r::3], np.broadcast_to(sel_ref[r], sel[r::3].shape))
+        assert np.array_equal(mindf[r::3], np.broadcast_to(mindf_ref[r], mindf[r::3].shape))
