@@ -28,8 +28,11 @@ Modules, each following the paper's definitions in its own notation:
 * ``rope``      -- rotary position embedding of query/key rows at their
                    preserved global positions (Appendix "RoPE Position ID
                    Assignment", sparse mode).
+* ``scorers``   -- the other chunk scorers (TF-IDF, BM25, Entropy) with
+                   exact scores rounded once to fp32, and the Even-Spaced
+                   token offsets (Appendix "Scoring Heuristic Details").
 
 Readings of points the paper leaves open are listed in each function's
 docstring.
 """
-from . import assembly, attention, cost, maxidf  # noqa: F401
+from . import assembly, attention, cost, maxidf, rope, scorers  # noqa: F401

@@ -13,6 +13,10 @@ described by the list of global positions, one per row.
 The Star Attention baseline prefixes the whole first block instead:
 Input_i = [B_0 || B_i] for i > 0 (Section 2 "Background").
 
+The Even-Spaced baseline (Appendix "Even-Spaced") keeps the same sink and
+summary slots, but Sigma_j is sigma = k * m single tokens of B_j at evenly
+spaced offsets (``scorers.even_spaced_offsets``) rather than k chunks.
+
 Readings taken: a chunk of Sigma_0 that overlaps the sink is kept as a
 duplicate row (Eq. 3 taken literally); block 0 gets no sink (Eq. 3).
 """
@@ -22,12 +26,14 @@ import numpy as np
 
 PREFIX_SUMMARY = 0
 PREFIX_ANCHOR = 1
+PREFIX_EVEN = 2
 
 
 def phase1_len(L: int, num_blocks: int, block_idx: int, sink: int, chunk: int, topk: int,
                mode: int = PREFIX_SUMMARY) -> int:
-    """Number of rows of Input_i, counted from Eq. 3 (summary mode: one block,
-    one sink, i summaries of k*m rows; anchor mode: two blocks)."""
+    """Number of rows of Input_i, counted from Eq. 3 (summary and Even-Spaced
+    modes: one block, one sink, i summaries of k*m rows; anchor mode: two
+    blocks)."""
     Lb = L // num_blocks
     if block_idx == 0:
         return Lb
@@ -47,6 +53,12 @@ def phase1_positions(L: int, num_blocks: int, block_idx: int, sink: int, chunk: 
     if i > 0:
         if mode == PREFIX_ANCHOR:
             segments.append(list(range(0, Lb)))                      # B_0
+        elif mode == PREFIX_EVEN:
+            from .scorers import even_spaced_offsets
+            segments.append(list(range(0, sink)))                    # S_sink
+            offs = even_spaced_offsets(Lb, topk * chunk)
+            for j in range(i):                                       # Sigma_j
+                segments.append([j * Lb + int(o) for o in offs])
         else:
             segments.append(list(range(0, sink)))                    # S_sink
             for j in range(i):                                       # Sigma_j
