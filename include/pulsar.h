@@ -48,6 +48,14 @@ typedef enum {
 
 typedef enum { PULSAR_OUT_F32 = 0, PULSAR_OUT_BF16 = 1 } pulsar_out_dtype;
 
+/* Chunk scorers (Appendix "Scoring Heuristic Details"). */
+typedef enum {
+  PULSAR_SCORE_MAXIDF = 0,  /* max over the chunk of IDF (Eq. maxidf) */
+  PULSAR_SCORE_TFIDF = 1,   /* mean over the chunk of IDF (Eq. tfidf) */
+  PULSAR_SCORE_BM25 = 2,    /* BM25 with k1 = 1.2, b = 0.75 (Eq. bm25) */
+  PULSAR_SCORE_ENTROPY = 3  /* distinct tokens / chunk length (Eq. entropy) */
+} pulsar_scorer;
+
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* pulsar_status_string(int status);
 
@@ -92,6 +100,39 @@ int pulsar_version(void);
 int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks,
                             int chunk, int topk, int vocab, int32_t* sel_chunks,
                             int32_t* chunk_mindf, float* idf, void* stream);
+
+/*
+ * Chunk summaries under any of the four scorers (Appendix "Scoring Heuristic
+ * Details": Corpus-Level IDF Table, TF-IDF, BM25, Entropy, Max-IDF).
+ *
+ * Blocks, df, IDF and chunks as for pulsar_maxidf_summaries.  For a chunk C
+ * of m tokens (tf(t) = occurrences of t in C):
+ *   MAXIDF   max over C of IDF(t);
+ *   TFIDF    (1/m) * sum over the positions of C of IDF(t);
+ *   BM25     sum over the distinct t of C of IDF_BM25(t) tf(t) (k1 + 1) /
+ *            (tf(t) + k1 D), IDF_BM25(t) = ln((N - df(t) + 0.5) /
+ *            (df(t) + 0.5) + 1), k1 = 1.2, b = 0.75, D = 1 - b + b m /
+ *            l_bar = 1 (all chunks have the mean length l_bar = m);
+ *   ENTROPY  (number of distinct tokens of C) / m.
+ * A score is computed in fp64 and rounded once to fp32, as the paper scores
+ * from an fp32 IDF table; the `topk` best chunks of each block (higher fp32
+ * score, then lower chunk index) are written in ascending chunk order.
+ * The chunk's tf comes from comparing each position with the whole chunk, so
+ * BM25 and ENTROPY cost O(m) per token.
+ *
+ * ids, sel_chunks  as for pulsar_maxidf_summaries.
+ * chunk_scores     out float [batch, num_blocks, Lb / chunk], nullable.
+ * scorer           a pulsar_scorer.
+ *
+ * EINVAL: as for pulsar_maxidf_summaries, or an unknown scorer.
+ * EUNSUPPORTED: num_blocks > 16, chunk not a power of two in [4, 256], or
+ *         the df table, chunk keys and (BM25, ENTROPY) a 16 KB staging area
+ *         do not fit in 160 KB of local data share (vocab up to about
+ *         130,000 at chunk 32 and L = 128K for BM25 and ENTROPY).
+ */
+int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                           int topk, int vocab, int scorer, int32_t* sel_chunks,
+                           float* chunk_scores, void* stream);
 
 /*
  * Number of rows n_i of block i's Phase-1 input (Eq. 3; Appendix

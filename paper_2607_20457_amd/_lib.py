@@ -19,6 +19,8 @@ SIGNATURES = {
     "pulsar_version": (_c_int, []),
     "pulsar_maxidf_summaries": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
                                          _vp, _vp, _vp, _vp]),
+    "pulsar_chunk_summaries": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
+                                        _c_int, _vp, _vp, _vp]),
     "pulsar_phase1_len": (_c_i64, [_c_i64, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),
     "pulsar_phase1_positions": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
                                          _c_int, _c_int, _vp, _vp]),

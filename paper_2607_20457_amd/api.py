@@ -17,6 +17,10 @@ PREFIX_SUMMARY = 0
 PREFIX_ANCHOR = 1
 OUT_F32 = 0
 OUT_BF16 = 1
+SCORE_MAXIDF = 0
+SCORE_TFIDF = 1
+SCORE_BM25 = 2
+SCORE_ENTROPY = 3
 
 
 def _stream():
@@ -58,6 +62,25 @@ def maxidf_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, 
     if return_idf:
         out.append(idf)
     return out[0] if len(out) == 1 else tuple(out)
+
+
+def chunk_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, vocab: int,
+                    scorer: int, return_scores: bool = False):
+    """Top-k chunks per block under a scorer (SCORE_*).  ids int32 [batch, L]
+    -> sel int32 [batch, num_blocks, topk] (+ fp32 scores [batch, N, C])."""
+    if ids.dim() == 1:
+        ids = ids[None]
+    _need(ids, torch.int32, "ids")
+    batch, L = ids.shape
+    C = (L // num_blocks) // chunk if num_blocks > 0 and chunk > 0 else 0
+    dev = ids.device
+    sel = torch.empty((batch, num_blocks, topk), dtype=torch.int32, device=dev)
+    scores = torch.empty((batch, num_blocks, C), dtype=torch.float32, device=dev) \
+        if return_scores else None
+    st = _lib.lib().pulsar_chunk_summaries(_ptr(ids), batch, L, num_blocks, chunk, topk, vocab,
+                                           scorer, _ptr(sel), _ptr(scores), _stream())
+    _lib.check(st, "pulsar_chunk_summaries")
+    return (sel, scores) if return_scores else sel
 
 
 def phase1_len(L: int, num_blocks: int, block_idx: int, sink: int, chunk: int, topk: int,

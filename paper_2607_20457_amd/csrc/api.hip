@@ -7,7 +7,7 @@
 
 namespace {
 
-constexpr int kVersion = 1;
+constexpr int kVersion = 2;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -94,6 +94,26 @@ int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_bl
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
   return launch_maxidf(ids, batch, L, num_blocks, chunk, topk, vocab, sel_chunks, chunk_mindf, idf,
                        lds, (hipStream_t)stream);
+}
+
+int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                           int topk, int vocab, int scorer, int32_t* sel_chunks,
+                           float* chunk_scores, void* stream) {
+  if (batch < 0 || L < 0 || num_blocks < 1 || vocab < 1 || chunk < 1 || topk < 0)
+    return PULSAR_EINVAL;
+  if (scorer < PULSAR_SCORE_MAXIDF || scorer > PULSAR_SCORE_ENTROPY) return PULSAR_EINVAL;
+  if (L % num_blocks != 0) return PULSAR_EINVAL;
+  const int64_t Lb = L / num_blocks;
+  if (Lb % chunk != 0 || topk > Lb / chunk) return PULSAR_EINVAL;
+  if ((int64_t)batch * L > 0 && (ids == nullptr || !aligned16(ids))) return PULSAR_EINVAL;
+  if ((int64_t)batch * num_blocks * topk > 0 && sel_chunks == nullptr) return PULSAR_EINVAL;
+  if (num_blocks > 16 || !is_pow2(chunk) || chunk < 4 || chunk > 256) return PULSAR_EUNSUPPORTED;
+  if (L >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
+  if (scorer_lds_bytes(L, num_blocks, chunk, vocab, scorer) > PULSAR_LDS_BYTES)
+    return PULSAR_EUNSUPPORTED;
+  if ((int64_t)batch * L == 0) return PULSAR_OK;
+  return launch_scorer(ids, batch, L, num_blocks, chunk, topk, vocab, scorer, sel_chunks,
+                       chunk_scores, (hipStream_t)stream);
 }
 
 int64_t pulsar_phase1_len(int64_t L, int num_blocks, int block_idx, int sink, int chunk, int topk,

@@ -106,6 +106,9 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
                   int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
                   hipStream_t stream);
 size_t maxidf_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab);
+int launch_scorer(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
+                  int vocab, int scorer, int32_t* sel, float* scores, hipStream_t stream);
+size_t scorer_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab, int scorer);
 
 int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
                      int n_rows, int32_t* pos, hipStream_t stream);

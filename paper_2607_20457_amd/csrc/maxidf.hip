@@ -37,10 +37,8 @@
 // A chunk's Max-IDF score ln(N / mindf) is strictly decreasing in mindf, so
 // ranking by (mindf ascending, index ascending) is ranking by (score
 // descending, index ascending).
-#include "common.hpp"
+#include "summary.hpp"
 
-#define MAXIDF_THREADS 1024
-#define MAXIDF_WAVES (MAXIDF_THREADS / PULSAR_WAVE)
 
 static inline int64_t round_up4(int64_t x) { return (x + 3) & ~int64_t(3); }
 
@@ -70,15 +68,6 @@ constexpr int kFastVocab = kFastWords * 32;
 constexpr int RES_ROUNDS = 16;
 constexpr int RES_ROUND_TOKENS = MAXIDF_THREADS * 8;
 constexpr int kResChunkBytes = PULSAR_LDS_BYTES - kFastVocab;
-
-// Stamp code: one byte per id, 16 * (15 - j) + (df - 1) after the id was
-// last seen in block j with df blocks so far (1 <= df <= j + 1 <= 16), or
-// kStampNever before it is first seen.  Once pass 1 is over the low nibble of
-// every seen id is df - 1 (stamp_to_df).
-constexpr int kStampMaxBlocks = 16;
-// word 3 of a buffer resource for raw 32-bit-offset access
-constexpr int kRawBuffer = 0x00020000;
-constexpr uint32_t kStampNever = 0xFFu;
 
 enum MaxidfMode { kGeneral = 0, kCompact = 1, kStamp = 2 };
 
@@ -169,77 +158,8 @@ __device__ __forceinline__ void mark_tokens_compact(const int (&t)[n], uint32_t 
     if (bit[i] & ~old[i]) atomicAdd(&dfw[ts[i] >> 2], 1u << ((ts[i] << 3) & 31));
 }
 
-// Stamp code, block j: an id whose byte is not yet stamped with j gets the
-// code of (df + 1, j).  With base = 16 * (15 - j), the codes stamped with j
-// are base .. base + j (df - 1 <= j); the code of an id last seen in an
-// earlier block, and kStampNever, lie above that range, and their low nibble
-// plus one (mod 16) is the new df - 1.  All lanes that write one byte during
-// block j write the same value, whatever order their loads and stores take,
-// so the count is exact without atomics as long as no two blocks run at once
-// (the caller puts a workgroup barrier between blocks).  PAD: the round holds
-// -1 padding, which stamps nothing.  An id at or above vocab is clamped into
-// the table (the caller's error).
-template <int n, bool PAD>
-__device__ __forceinline__ void stamp_tokens(const int (&t)[n], int j, uint32_t vmax,
-                                             uint8_t* code) {
-  uint32_t ts[n], c[n];
-#pragma unroll
-  for (int i = 0; i < n; ++i) ts[i] = min((uint32_t)t[i], vmax);
-#pragma unroll
-  for (int i = 0; i < n; ++i) c[i] = code[ts[i]];
-  const uint32_t base = 16u * (15u - (uint32_t)j);
-#pragma unroll
-  for (int i = 0; i < n; ++i) {
-    const bool stamped = c[i] - base <= (uint32_t)j;
-    if (!stamped && (!PAD || t[i] >= 0)) code[ts[i]] = (uint8_t)(base | ((c[i] + 1u) & 15u));
-  }
-}
-
-// After pass 1: every stamp code becomes df - 1 (its low nibble), four ids
-// per word.  Only ids never seen (kStampNever) read as df 16; no id of the
-// sequence is one of them.
-__device__ __forceinline__ void stamp_to_df(uint32_t* codew, int vocab_w4, int tid) {
-  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) codew[w] &= 0x0F0F0F0Fu;
-}
-
-// df of a stamp code after pass 1 (0 for an id never seen)
-__device__ __forceinline__ uint32_t stamp_df(uint32_t c) {
-  return c == kStampNever ? 0u : (c & 15u) + 1u;
-}
-
 __device__ __forceinline__ uint32_t df_of(int t, int vocab, const uint8_t* df8) {
   return df8[min((uint32_t)t, (uint32_t)(vocab - 1))];
-}
-
-// x moved across lanes by a DPP control (quad permutes, row mirrors)
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_mov(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
-}
-
-// Minimum over aligned groups of 2^GL lanes, the group size a compile-time
-// constant; every lane of a group ends with the group's minimum.
-template <int GL>
-__device__ __forceinline__ uint32_t group_min_c(uint32_t x) {
-  if (GL >= 1) x = min(x, dpp_mov<0xB1>(x));   // lane ^ 1
-  if (GL >= 2) x = min(x, dpp_mov<0x4E>(x));   // lane ^ 2
-  if (GL >= 3) x = min(x, dpp_mov<0x141>(x));  // mirror within 8
-  if (GL >= 4) x = min(x, dpp_mov<0x140>(x));  // mirror within 16
-  if (GL >= 5) x = min(x, (uint32_t)__shfl_xor((int)x, 16, 64));
-  if (GL >= 6) x = min(x, (uint32_t)__shfl_xor((int)x, 32, 64));
-  return x;
-}
-
-// Minimum over aligned groups of `group` lanes (a power of two); DPP within
-// rows of 16 lanes, cross-lane permutes beyond.
-__device__ __forceinline__ uint32_t group_min(uint32_t x, int group) {
-  if (group >= 2) x = min(x, dpp_mov<0xB1>(x));
-  if (group >= 4) x = min(x, dpp_mov<0x4E>(x));
-  if (group >= 8) x = min(x, dpp_mov<0x141>(x));
-  if (group >= 16) x = min(x, dpp_mov<0x140>(x));
-  if (group >= 32) x = min(x, (uint32_t)__shfl_xor((int)x, 16, 64));
-  if (group >= 64) x = min(x, (uint32_t)__shfl_xor((int)x, 32, 64));
-  return x;
 }
 
 // Optional IDF table (Eq. idf) of one sequence from its df bytes (STAMP:
@@ -251,76 +171,6 @@ __device__ void write_idf(const uint8_t* df8, int vocab, int num_blocks, float* 
   for (int t = tid; t < vocab; t += MAXIDF_THREADS) {
     const uint32_t d = STAMP ? stamp_df(df8[t]) : df8[t];
     out[t] = logf(n / (float)(d > 1u ? d : 1u));
-  }
-}
-
-// Lanes below this one with their bit set in a wave mask.
-__device__ __forceinline__ int count_below(uint64_t m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-}
-
-// Top-k chunks of one block from its chunk minima cv ([C] bytes in LDS),
-// written in ascending chunk order to dst.  Slot i of lane l is chunk
-// 64*i + l, so chunk order is (slot, lane) order and every count is a ballot.
-// The threshold tau is the smallest df with at least k chunks at or below it
-// (binary search over 1..N); every chunk below tau is kept, and the first
-// k - #(< tau) chunks equal to tau in chunk order.  S > 0: the block has at
-// most S slots and their values are held in registers; S == 0: any number of
-// slots, read from LDS each time.
-template <int S>
-__device__ __forceinline__ void select_block(const uint8_t* cv, int C, int num_blocks, int topk,
-                             int32_t* __restrict__ dst, int lane) {
-  const int slots = (C + 63) >> 6;
-  const int n_slots = S > 0 ? S : slots;
-  constexpr int R = S > 0 ? S : 1;
-  int xr[R];
-  // a lane past the last chunk holds 256, above every df (<= 255)
-#pragma unroll
-  for (int i = 0; i < R; ++i)
-    xr[i] = (S > 0 && i < slots && 64 * i + lane < C) ? (int)cv[64 * i + lane] : 256;
-#define SEL_X(i) \
-  (S > 0 ? xr[S > 0 ? (i) : 0] : (64 * (i) + lane < C ? (int)cv[64 * (i) + lane] : 256))
-  int lo = 0, hi = num_blocks;  // #(mindf <= lo) < k <= #(mindf <= hi)
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    int cnt = 0;
-#pragma unroll
-    for (int i = 0; i < n_slots; ++i) cnt += __popcll(__ballot(SEL_X(i) <= mid));
-    if (cnt >= topk) hi = mid; else lo = mid;
-  }
-  const int tau = hi;
-  int n_lt = 0;
-#pragma unroll
-  for (int i = 0; i < n_slots; ++i) n_lt += __popcll(__ballot(SEL_X(i) < tau));
-  const int need = topk - n_lt;  // kept chunks equal to tau
-  int eq_before = 0, out_before = 0;
-#pragma unroll
-  for (int i = 0; i < n_slots; ++i) {
-    const int x = SEL_X(i);
-    const uint64_t m_eq = __ballot(x == tau);
-    const bool keep = x < tau || (x == tau && eq_before + count_below(m_eq) < need);
-    const uint64_t m_keep = __ballot(keep);
-    if (keep) dst[out_before + count_below(m_keep)] = 64 * i + lane;
-    eq_before += __popcll(m_eq);
-    out_before += __popcll(m_keep);
-  }
-#undef SEL_X
-}
-
-// Top-k chunks of every block of sequence b from the chunk minima cmin
-// ([num_blocks][C] bytes in LDS); one wavefront per block.
-__device__ __forceinline__ void select_topk(const uint8_t* cmin, int64_t b, int num_blocks, int C,
-                                            int topk, int32_t* __restrict__ sel, int wave,
-                                            int lane) {
-  if (topk == 0) return;
-  // the block loop is uniform across the wavefront: keep it scalar
-  for (int j = __builtin_amdgcn_readfirstlane(wave); j < num_blocks; j += MAXIDF_WAVES) {
-    const uint8_t* cv = cmin + (int64_t)j * C;
-    int32_t* dst = sel + (b * num_blocks + j) * topk;
-    if (C <= 4 * 64)
-      select_block<4>(cv, C, num_blocks, topk, dst, lane);
-    else
-      select_block<0>(cv, C, num_blocks, topk, dst, lane);
   }
 }
 
@@ -478,7 +328,7 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   __syncthreads();
 
   // ---- select ------------------------------------------------------------
-  select_topk(cmin, b, num_blocks, Lb >> chunk_log2, topk, sel, wave, lane);
+  select_topk(cmin, b, num_blocks, Lb >> chunk_log2, (uint32_t)num_blocks, topk, sel, wave, lane);
 }
 
 // Register-resident variant with the stamp code when the sequence fits the
@@ -644,7 +494,8 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
       }
     }
     __syncthreads();
-    select_topk(cmin, b, num_blocks, (int)(L / num_blocks) >> chunk_log2, topk, sel, wave, lane);
+    select_topk(cmin, b, num_blocks, (int)(L / num_blocks) >> chunk_log2, (uint32_t)num_blocks, topk,
+                sel, wave, lane);
   }
 }
 

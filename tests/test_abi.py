@@ -177,3 +177,20 @@ def test_phase2_query_validation():
     assert call(ws=None) == EWS
     assert call(wsb=ws_need - 1) == EWS
     assert call(Tq=0) == 0
+
+
+def test_chunk_summaries_validation():
+    f = _lib.lib().pulsar_chunk_summaries
+    def call(ids=FAKE, batch=1, L=4096, N=4, m=16, k=4, V=1000, scorer=1, sel=FAKE):
+        return f(ids, batch, L, N, m, k, V, scorer, sel, None, None)
+    assert call(scorer=4) == EINVAL and call(scorer=-1) == EINVAL
+    assert call(L=4097) == EINVAL          # L % N
+    assert call(m=24) == EINVAL            # Lb % m
+    assert call(k=65) == EINVAL            # k > Lb / m
+    assert call(ids=None) == EINVAL
+    assert call(ids=FAKE + 4) == EINVAL    # misaligned
+    assert call(sel=None) == EINVAL
+    assert call(N=32, L=4096) == EUNSUP    # more than 16 blocks
+    assert call(m=512, L=8192, k=1) == EUNSUP
+    assert call(L=131072, N=16, m=32, k=4, V=150000, scorer=2) == EUNSUP  # LDS
+    assert call(batch=0, ids=None, sel=None) == 0
