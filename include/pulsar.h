@@ -43,7 +43,11 @@ typedef enum {
   /* Input_i = [S_sink || Sigma_0 || ... || Sigma_{i-1} || B_i] (Eq. 3) */
   PULSAR_PREFIX_SUMMARY = 0,
   /* Star Attention anchor baseline: Input_i = [B_0 || B_i] (Section 2) */
-  PULSAR_PREFIX_ANCHOR = 1
+  PULSAR_PREFIX_ANCHOR = 1,
+  /* Even-Spaced baseline (Appendix "Even-Spaced"): Eq. 3 with Sigma_j the
+     sigma = topk * chunk positions j*Lb + floor(r (Lb - 1) / (sigma - 1)),
+     r = 0 .. sigma - 1 (position j*Lb alone when sigma = 1); no sel_chunks */
+  PULSAR_PREFIX_EVEN = 2
 } pulsar_prefix_mode;
 
 typedef enum { PULSAR_OUT_F32 = 0, PULSAR_OUT_BF16 = 1 } pulsar_out_dtype;
@@ -137,8 +141,8 @@ int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blo
 /*
  * Number of rows n_i of block i's Phase-1 input (Eq. 3; Appendix
  * "Block-to-Host Scalability Analysis"):
- *   block 0: Lb;  summary mode: Lb + sink + block_idx * topk * chunk;
- *   anchor mode (block_idx > 0): 2 * Lb.
+ *   block 0: Lb;  summary and Even-Spaced modes: Lb + sink + block_idx *
+ *   topk * chunk;  anchor mode (block_idx > 0): 2 * Lb.
  * Returns n_i >= 0, or a negative pulsar_status on invalid arguments
  * (L % num_blocks != 0, block_idx outside [0, num_blocks), sink > Lb,
  * topk * chunk > Lb, negative sizes, unknown mode).  Host-only; no GPU call.
@@ -152,11 +156,14 @@ int64_t pulsar_phase1_len(int64_t L, int num_blocks, int block_idx, int sink, in
  * Assignment").  Rows [0, sink) are positions 0..sink-1; then for every
  * earlier block j < i and every selected chunk c of Sigma_j (in the order of
  * sel_chunks) the m positions j*Lb + c*m + r; then block i's own positions
- * i*Lb + r.  Block 0 is [B_0] alone; anchor mode is [B_0 || B_i].
+ * i*Lb + r.  Block 0 is [B_0] alone; anchor mode is [B_0 || B_i]; the
+ * Even-Spaced mode replaces each Sigma_j by its sigma = topk * chunk evenly
+ * spaced positions (see PULSAR_PREFIX_EVEN).
  *
  * sel_chunks  int32 [batch, num_blocks, topk] (as written by
- *             pulsar_maxidf_summaries); only blocks < block_idx are read;
- *             may be NULL in anchor mode, when block_idx == 0 or topk == 0.
+ *             pulsar_maxidf_summaries or pulsar_chunk_summaries); only
+ *             blocks < block_idx are read; may be NULL in the anchor and
+ *             Even-Spaced modes, when block_idx == 0 or topk == 0.
  *             Chunk indices must lie in [0, Lb / chunk).
  * pos         out int32 [batch, n_i].
  * Errors: as pulsar_phase1_len, plus EINVAL for NULL pointers, batch < 0,

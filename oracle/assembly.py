@@ -56,7 +56,7 @@ def phase1_positions(L: int, num_blocks: int, block_idx: int, sink: int, chunk: 
         elif mode == PREFIX_EVEN:
             from .scorers import even_spaced_offsets
             segments.append(list(range(0, sink)))                    # S_sink
-            offs = even_spaced_offsets(Lb, topk * chunk)
+            offs = even_spaced_offsets(Lb, topk * chunk) if topk * chunk else []
             for j in range(i):                                       # Sigma_j
                 segments.append([j * Lb + int(o) for o in offs])
         else:

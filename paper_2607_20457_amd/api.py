@@ -15,6 +15,7 @@ from . import _lib
 
 PREFIX_SUMMARY = 0
 PREFIX_ANCHOR = 1
+PREFIX_EVEN = 2
 OUT_F32 = 0
 OUT_BF16 = 1
 SCORE_MAXIDF = 0

@@ -17,7 +17,8 @@ int64_t phase1_len_checked(int64_t L, int num_blocks, int block_idx, int sink, i
                            int prefix_mode) {
   if (L < 0 || num_blocks < 1 || L % num_blocks != 0) return PULSAR_EINVAL;
   if (block_idx < 0 || block_idx >= num_blocks) return PULSAR_EINVAL;
-  if (prefix_mode != PULSAR_PREFIX_SUMMARY && prefix_mode != PULSAR_PREFIX_ANCHOR)
+  if (prefix_mode != PULSAR_PREFIX_SUMMARY && prefix_mode != PULSAR_PREFIX_ANCHOR &&
+      prefix_mode != PULSAR_PREFIX_EVEN)
     return PULSAR_EINVAL;
   const int64_t Lb = L / num_blocks;
   if (sink < 0 || sink > Lb) return PULSAR_EINVAL;
@@ -44,6 +45,12 @@ RowMap make_map(int64_t L, int num_blocks, int block_idx, int sink, int chunk, i
     mp.offset = 0;
   } else if (prefix_mode == PULSAR_PREFIX_ANCHOR) {
     mp.mode = MAP_ANCHOR;
+  } else if (prefix_mode == PULSAR_PREFIX_EVEN) {
+    mp.mode = MAP_EVEN;
+    mp.sigma = topk * chunk;
+    mp.prefix = block_idx * mp.sigma;
+    mp.inv_sigma = mp.sigma > 0 ? 1.0f / (float)mp.sigma : 0.f;
+    mp.inv_sigma1 = mp.sigma > 1 ? 1.0 / (double)(mp.sigma - 1) : 0.0;
   } else {
     mp.mode = MAP_SUMMARY;
     mp.n_runs = block_idx * topk;

@@ -22,7 +22,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // positions, one run per selected chunk; run q = j*k + c starts at
 // j*Lb + sel[j][c]*m.  Kernels stage these run starts in LDS once
 // (build_run_table) and then map a row with a few integer operations.
-enum MapMode : int { MAP_IDENTITY = 0, MAP_SUMMARY = 1, MAP_ANCHOR = 2 };
+enum MapMode : int { MAP_IDENTITY = 0, MAP_SUMMARY = 1, MAP_ANCHOR = 2, MAP_EVEN = 3 };
 
 struct RowMap {
   int mode;
@@ -37,6 +37,9 @@ struct RowMap {
   int m_log2;      // log2(m) when m is a power of two, else -1
   float inv_chunk; // 1 / m
   int64_t offset;  // identity mode: position of row 0
+  int sigma;           // Even-Spaced: points per earlier block, k * m
+  float inv_sigma;     // 1 / sigma
+  double inv_sigma1;   // 1 / (sigma - 1), sigma > 1
 };
 
 // run_base[q] = j*Lb + sel[j][c]*m for run q = j*k + c; a selection outside
@@ -59,6 +62,26 @@ __device__ __forceinline__ int row_position(const RowMap& mp, const int* run_bas
   if (r < mp.sink) return r;
   const int t = r - mp.sink;
   if (t >= mp.prefix) return mp.block_idx * mp.Lb + (t - mp.prefix);
+  if (mp.mode == MAP_EVEN) {
+    // point p of block j: j*Lb + floor(p (Lb - 1) / (sigma - 1)); both
+    // quotients are estimated in floating point and corrected exactly
+    const int sig = mp.sigma;
+    int j = (int)((float)t * mp.inv_sigma);
+    int p = t - j * sig;
+    if (p < 0) {
+      --j;
+      p += sig;
+    } else if (p >= sig) {
+      ++j;
+      p -= sig;
+    }
+    if (sig == 1) return j * mp.Lb;
+    const int64_t num = (int64_t)p * (mp.Lb - 1);  // < 2^48: exact as a double
+    int64_t off = (int64_t)((double)num * mp.inv_sigma1);
+    if (off * (sig - 1) > num) --off;
+    else if ((off + 1) * (sig - 1) <= num) ++off;
+    return j * mp.Lb + (int)off;
+  }
   int q, w;
   if (mp.m_log2 >= 0) {
     q = t >> mp.m_log2;

@@ -47,7 +47,7 @@ def test_status_strings_and_version():
 @pytest.mark.parametrize("L,N,i,s,m,k,mode", [
     (4096, 4, 3, 64, 16, 4, 0), (32768, 8, 7, 64, 32, 16, 0), (131072, 16, 15, 64, 32, 32, 0),
     (131072, 16, 15, 64, 32, 32, 1), (131072, 16, 0, 64, 32, 32, 0), (1024, 4, 2, 0, 8, 0, 0),
-    (1024, 4, 3, 256, 8, 32, 0)])
+    (1024, 4, 3, 256, 8, 32, 0), (131072, 16, 15, 64, 32, 32, 2), (1000, 4, 3, 7, 5, 3, 2)])
 def test_phase1_len_matches_oracle(L, N, i, s, m, k, mode):
     got = _lib.lib().pulsar_phase1_len(L, N, i, s, m, k, mode)
     assert got == assembly.phase1_len(L, N, i, s, m, k, mode)
@@ -60,6 +60,7 @@ def test_phase1_len_matches_oracle(L, N, i, s, m, k, mode):
     (4096, 4, 1, 64, 16, 65, 0),    # k * m > Lb
     (4096, 4, 1, 64, 0, 1, 0),      # chunk 0
     (4096, 4, 1, 64, 16, 1, 7),     # mode
+    (4096, 4, 1, 64, 16, 1, 3),     # mode
     (4096, 0, 0, 0, 16, 1, 0),      # no blocks
 ])
 def test_phase1_len_rejects(args):

@@ -27,7 +27,8 @@ def _run(cfg, i, mode, sel, q, k, v, o_dtype=P.OUT_F32, keep=False):
     print(f"phase1 parity: {cfg.name} block={i} mode={mode} q={q.shape} o_dtype={o_dtype}",
           flush=True)
     res = P.phase1_attn(to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), cfg.num_blocks, i,
-                        cfg.sink, cfg.chunk, cfg.topk, to_dev_i32(sel), mode, o_dtype=o_dtype,
+                        cfg.sink, cfg.chunk, cfg.topk, None if sel is None else to_dev_i32(sel),
+                        mode, o_dtype=o_dtype,
                         keep_kv=keep)
     torch.cuda.synchronize()
     return res
@@ -36,7 +37,7 @@ def _run(cfg, i, mode, sel, q, k, v, o_dtype=P.OUT_F32, keep=False):
 def _full_check(cfg, i, mode, sel, q, k, v, b=0):
     o, lse = _run(cfg, i, mode, sel, q, k, v)
     pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk,
-                                    sel[b], mode)
+                                    None if sel is None else sel[b], mode)
     o_ref, lse_ref = attention.phase1_attention(f64(q[b]), f64(k[b]), f64(v[b]), pos,
                                                 1 / math.sqrt(cfg.d))
     check_attention(o[b].cpu().numpy(), lse[b].cpu().numpy(), o_ref, lse_ref,
@@ -46,7 +47,7 @@ def _full_check(cfg, i, mode, sel, q, k, v, b=0):
 def _sampled_check(cfg, i, mode, sel, q, k, v, rows, b=0):
     o, lse = _run(cfg, i, mode, sel, q, k, v)
     pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk,
-                                    sel[b], mode)
+                                    None if sel is None else sel[b], mode)
     rows = np.array(sorted(set(int(r) for r in rows if 0 <= r < len(pos))))
     o_ref, lse_ref = attention.phase1_attention(f64(q[b]), f64(k[b]), f64(v[b]), pos,
                                                 1 / math.sqrt(cfg.d), rows=rows)
@@ -158,3 +159,32 @@ def test_far_larger_later_score_takes_exact_pass():
     sel = np.array([[[0, 5], [1, 2]]], dtype=np.int32)
     _full_check(cfg, 0, P.PREFIX_SUMMARY, sel, q, k, v)
     _full_check(cfg, 1, P.PREFIX_SUMMARY, sel, q, k, v)
+
+
+def test_even_spaced_prefix_tiny_full():
+    # Even-Spaced baseline: Sigma_j = k*m evenly spaced tokens of B_j
+    cfg = workload.CONFIGS["tiny"]
+    sel, q, k, v = _inputs(cfg)
+    for i in range(cfg.num_blocks):
+        _full_check(cfg, i, P.PREFIX_EVEN, None, q, k, v)
+
+
+def test_even_spaced_prefix_128k_block15_sampled():
+    cfg = workload.CONFIGS["llama8b_128k"]
+    _, q, k, v = _inputs(cfg)
+    n = P.phase1_len(cfg.L, cfg.num_blocks, 15, cfg.sink, cfg.chunk, cfg.topk, P.PREFIX_EVEN)
+    sigma = cfg.topk * cfg.chunk
+    rows = [0, 63, 64, 64 + sigma - 1, 64 + sigma, 64 + 7 * sigma + 5, n - 8193, n - 8192,
+            n - 1] + list(np.random.default_rng(3).integers(0, n, 120))
+    _sampled_check(cfg, 15, P.PREFIX_EVEN, None, q, k, v, rows)
+
+
+@pytest.mark.parametrize("Lb,sink,m,k", [(1024, 64, 16, 4), (1000, 10, 20, 7), (4096, 0, 32, 16),
+                                         (777, 5, 1, 1), (256, 3, 8, 0)])
+def test_even_spaced_positions_match_the_oracle(Lb, sink, m, k):
+    N = 5
+    for i in range(N):
+        pos = P.phase1_positions(None, 2, N * Lb, N, i, sink, m, k, P.PREFIX_EVEN,
+                                 device="cuda").cpu().numpy()
+        ref = assembly.phase1_positions(N * Lb, N, i, sink, m, k, None, assembly.PREFIX_EVEN)
+        assert np.array_equal(pos[0], ref) and np.array_equal(pos[1], ref)
