@@ -206,6 +206,36 @@ def run_main(args):
     torch.cuda.synchronize()
     del big
 
+    # The other chunk scorers over the same sequence (batch 1, latency-bound
+    # on one compute unit) and over 256 copies of it (one per compute unit)
+    scorer_rows = {}
+    big = d_ids.expand(256, cfg.L).contiguous()
+    for name, sc in (("tfidf", P.SCORE_TFIDF), ("bm25", P.SCORE_BM25),
+                     ("entropy", P.SCORE_ENTROPY)):
+        row = {}
+        for batch, inp in ((1, d_ids), (256, big)):
+            t = Timer()
+            P.chunk_summaries(inp, N, cfg.chunk, cfg.topk, cfg.vocab, sc)
+            for _ in range(5):
+                with t:
+                    P.chunk_summaries(inp, N, cfg.chunk, cfg.topk, cfg.vocab, sc)
+            torch.cuda.synchronize()
+            row[f"batch{batch}_ms"] = t.mean_ms()
+            row[f"batch{batch}_tokens_per_s"] = batch * cfg.L / (t.mean_ms() * 1e-3)
+        scorer_rows[name] = row
+    del big
+
+    # Phase 1 of block 15 with the Even-Spaced baseline prefix (same row count)
+    t_even = Timer()
+    for _ in range(2):
+        P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, None, P.PREFIX_EVEN,
+                      out=O, return_lse=False)
+    for _ in range(5):
+        with t_even:
+            P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, None,
+                          P.PREFIX_EVEN, out=O, return_lse=False)
+    torch.cuda.synchronize()
+
     # Rotary embedding of the layer's Q and K at their global positions (the
     # sparse-position mode), once per layer for the whole context; on copies,
     # so that the attention inputs above stay as drawn
@@ -293,6 +323,8 @@ def run_main(args):
                 "decode_kv_gbps": kv_bytes / (t_dec.mean_ms() * 1e-3) / 1e9,
                 "decode_pct_hbm_peak": 100 * kv_bytes / (t_dec.mean_ms() * 1e-3) / 1e9 / PEAK_HBM_GBPS,
             },
+            "scorers": scorer_rows,
+            "even_spaced_phase1_ms": t_even.mean_ms(),
             "phase2_partial_merge_ms": p2_ms,
             "phase2_tflops": f_p2 / (p2_ms * 1e-3) / 1e12,
             "phase2_gbps_algorithmic": p2_bytes / (p2_ms * 1e-3) / 1e9,
