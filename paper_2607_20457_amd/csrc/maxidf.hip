@@ -335,9 +335,10 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
 // register file: L = ROUNDS * 8192 with ROUNDS a power of two up to 16, and
 // Lb a multiple of 8192, so that every thread owns exactly ROUNDS x 2
 // 16-byte groups of ids.  Pass 1 keeps each thread's ids in registers and
-// pass 2 reads them back from there: the ids cross HBM once.  Thread tid's
-// group u of round rd is the sequence's 16-byte group (2*rd + u)*1024 + tid,
-// which is also the group pass 2 assigns to slot 2*rd + u.
+// pass 2 reads them back from there: the ids cross HBM once.  In round rd
+// thread tid holds the 8 consecutive ids (rd*1024 + tid)*8 .. +7 (two
+// adjacent 16-byte groups), so a chunk of m >= 8 ids spans m/8 lanes and
+// pass 2 takes half of its minimum within the lane.
 //
 // Packing of the 4 clamped ids (< 2^17) of slot s: their low 16 bits two per
 // register (plo), and their bit 16 in byte i of hb[s / 8] at bit s % 8 --
@@ -377,10 +378,9 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
   uint8_t* cmin = lds8 + kFastVocab;
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const int vocab_w4 = (vocab + 3) >> 2;
-  const uint32_t lane_off = (uint32_t)tid * 16u;
-  const int group_log2 = GL >= 0 ? GL : chunk_log2 - 2;  // lanes per chunk: 1..64
-  const int group = 1 << group_log2;
-  const int nchunks_seq = (int)(L >> (group_log2 + 2));
+  const uint32_t lane_off = (uint32_t)tid * 32u;
+  const int cl2 = GL >= 0 ? GL + 2 : chunk_log2;  // log2(chunk)
+  const int nchunks_seq = (int)(L >> cl2);
 
   // a sequence's ids through a buffer resource (no bytes past the batch):
   // one lane offset, and each group's offset a scalar constant
@@ -391,8 +391,8 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
   auto load_round = [&](__amdgpu_buffer_rsrc_t r, int rd, int4 (&t)[2]) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const auto v =
-          __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, (2 * rd + u) * MAXIDF_THREADS * 16, 0);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(
+          r, lane_off, rd * MAXIDF_THREADS * 32 + u * 16, 0);
       t[u] = make_int4((int)v[0], (int)v[1], (int)v[2], (int)v[3]);
     }
   };
@@ -467,29 +467,45 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
     int tid_i = tid;
     asm volatile("" : "+v"(tid_i));
 #pragma unroll
-    for (int slot = 0; slot < 2 * ROUNDS; ++slot) {
-      const uint32_t lo0 = plo[slot >> 1][slot & 1][0], lo1 = plo[slot >> 1][slot & 1][1];
-      const uint32_t x = (hb[slot >> 3] >> (slot & 7)) & 0x01010101u;
-      const uint32_t t0 = __builtin_amdgcn_perm(x, lo0, 0x0C040100u);
-      const uint32_t t1 = __builtin_amdgcn_perm(x, lo0, 0x0C050302u);
-      const uint32_t t2 = __builtin_amdgcn_perm(x, lo1, 0x0C060100u);
-      const uint32_t t3 = __builtin_amdgcn_perm(x, lo1, 0x0C070302u);
-      // the table holds df - 1
-      uint32_t mn = min(min((uint32_t)code8[t0], (uint32_t)code8[t1]),
-                        min((uint32_t)code8[t2], (uint32_t)code8[t3]));
-      if constexpr (GL >= 0) mn = group_min_c<GL>(mn);
-      else mn = group_min(mn, group);
-      mn += 1u;
-      if ((tid_i & (group - 1)) == 0) {
-        const int c = (slot * MAXIDF_THREADS + tid_i) >> group_log2;
-        cmin[c] = (uint8_t)mn;
-        if (chunk_mindf) chunk_mindf[b * nchunks_seq + c] = (int32_t)mn;
+    for (int rd = 0; rd < ROUNDS; ++rd) {
+      // the minimum df - 1 of each 16-byte half of the lane's 8 ids
+      uint32_t mn[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int slot = 2 * rd + u;
+        const uint32_t lo0 = plo[rd][u][0], lo1 = plo[rd][u][1];
+        const uint32_t x = (hb[slot >> 3] >> (slot & 7)) & 0x01010101u;
+        const uint32_t t0 = __builtin_amdgcn_perm(x, lo0, 0x0C040100u);
+        const uint32_t t1 = __builtin_amdgcn_perm(x, lo0, 0x0C050302u);
+        const uint32_t t2 = __builtin_amdgcn_perm(x, lo1, 0x0C060100u);
+        const uint32_t t3 = __builtin_amdgcn_perm(x, lo1, 0x0C070302u);
+        mn[u] = min(min((uint32_t)code8[t0], (uint32_t)code8[t1]),
+                    min((uint32_t)code8[t2], (uint32_t)code8[t3]));
       }
-      // every fourth slot frees two rounds of packed ids: load one round of
+      const int g8 = rd * MAXIDF_THREADS + tid_i;  // the lane's 8-id group in the sequence
+      if (cl2 == 2) {
+        // chunks of 4 ids: each half is a chunk of its own
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          cmin[2 * g8 + u] = (uint8_t)(mn[u] + 1u);
+          if (chunk_mindf) chunk_mindf[b * nchunks_seq + 2 * g8 + u] = (int32_t)(mn[u] + 1u);
+        }
+      } else {
+        const int lg = cl2 - 3;  // log2 of the lanes per chunk, m / 8
+        uint32_t m2 = min(mn[0], mn[1]);
+        if constexpr (GL >= 1) m2 = group_min_c<GL - 1>(m2);
+        else m2 = group_min(m2, 1 << lg);
+        m2 += 1u;
+        if ((tid_i & ((1 << lg) - 1)) == 0) {
+          cmin[g8 >> lg] = (uint8_t)m2;
+          if (chunk_mindf) chunk_mindf[b * nchunks_seq + (g8 >> lg)] = (int32_t)m2;
+        }
+      }
+      // every second round frees two rounds of packed ids: load one round of
       // the next sequence in their place
-      if ((slot & 3) == 3 && (slot >> 2) < CARRY) {
+      if ((rd & 1) == 1 && (rd >> 1) < CARRY) {
         __builtin_amdgcn_sched_barrier(0);
-        load_round(rnext, slot >> 2, nbuf[(slot >> 2) < CARRY ? (slot >> 2) : 0]);
+        load_round(rnext, rd >> 1, nbuf[(rd >> 1) < CARRY ? (rd >> 1) : 0]);
         __builtin_amdgcn_sched_barrier(0);
       }
     }

@@ -47,8 +47,20 @@ __device__ __forceinline__ void stamp_tokens(const int (&t)[n], int j, uint32_t 
 // After pass 1: every stamp code becomes df - 1 (its low nibble), four ids
 // per word.  Only ids never seen (kStampNever) read as df 16; no id of the
 // sequence is one of them.
+// The table starts 16-byte aligned; 16 bytes per access, then the words past
+// the last full 16 bytes.
 __device__ __forceinline__ void stamp_to_df(uint32_t* codew, int vocab_w4, int tid) {
-  for (int w = tid; w < vocab_w4; w += MAXIDF_THREADS) codew[w] &= 0x0F0F0F0Fu;
+  uint4* c16 = reinterpret_cast<uint4*>(codew);
+  const int n16 = vocab_w4 >> 2;
+  for (int w = tid; w < n16; w += MAXIDF_THREADS) {
+    uint4 x = c16[w];
+    x.x &= 0x0F0F0F0Fu;
+    x.y &= 0x0F0F0F0Fu;
+    x.z &= 0x0F0F0F0Fu;
+    x.w &= 0x0F0F0F0Fu;
+    c16[w] = x;
+  }
+  for (int w = 4 * n16 + tid; w < vocab_w4; w += MAXIDF_THREADS) codew[w] &= 0x0F0F0F0Fu;
 }
 
 // df of a stamp code after pass 1 (0 for an id never seen)
