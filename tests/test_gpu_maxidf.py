@@ -148,3 +148,18 @@ def test_batch_beyond_compute_units(L, N, batch, m):
     for r in range(3):
         assert np.array_equal(sel[r::3], np.broadcast_to(sel_ref[r], sel[r::3].shape))
         assert np.array_equal(mindf[r::3], np.broadcast_to(mindf_ref[r], mindf[r::3].shape))
+
+
+@pytest.mark.parametrize("L,N,m,V,layout", [
+    (32 * 1024, 32, 16, 32000, "compact bitmaps (N > 16)"),
+    (64 * 2048, 64, 32, 128256, "compact bitmaps, 64 blocks"),
+    (20 * 1024, 20, 32, 140000, "general bitmaps (vocab > 131072)"),
+    (3 * 8192, 3, 32, 128256, "stamp code, streaming (3 rounds)"),
+    (12 * 4096, 12, 16, 50000, "stamp code, streaming (blocks of 4096)"),
+    (2 * 8192, 2, 8, 1000, "stamp code, resident (2 rounds)"),
+])
+def test_every_kernel_layout(L, N, m, V, layout):
+    # one case per df-counting layout the host plan can pick
+    ids = workload.zipf_ids(3000 + N + m, L, V)[None]
+    print(f"maxidf layout: {layout}", flush=True)
+    _check(ids, N, m, min(5, L // N // m), V)
