@@ -209,8 +209,9 @@ int pulsar_phase1_attn(const void* Q, const void* K, const void* V, int batch, i
 // Phase-2 key splitting: each shard is cut into nsplit ranges so that the
 // launch has enough workgroups to cover the chip; the partials of a shard are
 // then merged with the same online-softmax merge as the shards themselves.
-static int phase2_splits(int n_shards, int Tq, int64_t S, int Hq, int Hkv) {
+static int phase2_splits(int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d) {
   if (S <= 0) return 1;
+  if (decode_applies(Tq, Hq, Hkv, d)) return decode_parts(n_shards, S, Hkv);
   const int group = Hq / Hkv;
   const int heads_per_wg = group >= 4 ? 4 : group;
   const int rows_per_wg = attn_rows_per_wg(group, false);
@@ -229,7 +230,7 @@ extern "C" {
 
 size_t pulsar_phase2_workspace_bytes(int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d) {
   if (n_shards < 0 || Tq < 0 || S < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1) return 0;
-  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv);
+  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv, d);
   if (ns <= 1) return 0;
   const int64_t per = (int64_t)n_shards * ns;
   return (size_t)(per * Tq * Hq * d * 4 + per * Hq * Tq * 4);
@@ -252,10 +253,23 @@ int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_sha
   if (S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;
   if (!aligned16(q) || (S > 0 && (!aligned16(K) || !aligned16(V))) || !aligned16(o_parts))
     return PULSAR_EINVAL;
-  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv);
+  const int ns = phase2_splits(n_shards, Tq, S, Hq, Hkv, d);
   const size_t need = pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need || !aligned16(workspace)))
     return PULSAR_EWORKSPACE;
+
+  float* ws_o = static_cast<float*>(workspace);
+  float* ws_l = ws_o + (int64_t)n_shards * ns * Tq * Hq * d;
+  if (decode_applies(Tq, Hq, Hkv, d)) {
+    // few query rows: the decode kernel, one key range per wave
+    int st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(K),
+                           static_cast<const uint16_t*>(V), n_shards, Tq, S, Hq, Hkv, d,
+                           softmax_scale, ns > 1 ? ws_o : o_parts, ns > 1 ? ws_l : lse_parts, ns,
+                           (hipStream_t)stream);
+    if (st != PULSAR_OK || ns == 1) return st;
+    return launch_lse_merge(ws_o, ws_l, ns, n_shards, Tq, Hq, d, (int64_t)Tq * Hq * d,
+                            (int64_t)Hq * Tq, o_parts, lse_parts, (hipStream_t)stream);
+  }
 
   AttnLaunch a{};
   a.Q = static_cast<const uint16_t*>(q);
@@ -279,8 +293,6 @@ int pulsar_phase2_partial(const void* q, const void* K, const void* V, int n_sha
   a.o_bf16 = 0;
   a.o_zstride = (int64_t)Tq * Hq * d;
   a.lse_zstride = (int64_t)Hq * Tq;
-  float* ws_o = static_cast<float*>(workspace);
-  float* ws_l = ws_o + (int64_t)n_shards * ns * Tq * Hq * d;
   a.O = ns > 1 ? ws_o : o_parts;
   a.lse = ns > 1 ? ws_l : lse_parts;
   int st = launch_attention(a, (hipStream_t)stream);

@@ -129,6 +129,11 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
                   int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
                   hipStream_t stream);
 size_t maxidf_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab);
+int decode_parts(int n_shards, int64_t S, int Hkv);
+bool decode_applies(int Tq, int Hq, int Hkv, int d);
+int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n_shards, int Tq,
+                  int64_t S, int Hq, int Hkv, int d, float scale, float* o, float* lse,
+                  int nparts, hipStream_t stream);
 int launch_scorer(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
                   int vocab, int scorer, int32_t* sel, float* scores, hipStream_t stream);
 size_t scorer_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab, int scorer);

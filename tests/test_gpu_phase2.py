@@ -122,3 +122,39 @@ def test_phase2_far_larger_later_score():
     for h in range(2):
         ref = attention.partial_attention(f64(qb), f64(kb[h]), f64(vb[h]), 1 / math.sqrt(d))
         check_attention(o_parts[h].cpu().numpy(), lse_parts[h].cpu().numpy(), *ref, f"shard {h}")
+
+
+@pytest.mark.parametrize("Tq,H,S,Hq,Hkv,d", [
+    (1, 2, 1, 32, 8, 128),      # one key
+    (1, 3, 31, 32, 8, 128),     # one partial step
+    (2, 2, 33, 16, 8, 64),      # group 2, a step and one key
+    (4, 5, 1000, 32, 4, 128),   # group 8: 32 packed rows
+    (8, 1, 4100, 8, 2, 64),     # group 4, 32 packed rows, many key ranges
+    (3, 4, 777, 8, 8, 128),     # group 1
+])
+def test_decode_kernel_shapes(Tq, H, S, Hq, Hkv, d):
+    # few query rows per KV head (Tq * Hq / Hkv <= 32): the decode kernel,
+    # one key range per wave, merged per shard
+    print(f"decode parity: Tq={Tq} shards={H} S={S} Hq={Hq} Hkv={Hkv} d={d}", flush=True)
+    q = workload.bf16_normal(40 + Tq + S, (Tq, Hq, d))
+    k, v = _shards(H, S, Hkv, d, 41 + S)
+    o_parts, lse_parts = P.phase2_partial(to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v))
+    torch.cuda.synchronize()
+    for h in range(H):
+        ref = attention.partial_attention(f64(q), f64(k[h]), f64(v[h]), 1 / math.sqrt(d))
+        check_attention(o_parts[h].cpu().numpy(), lse_parts[h].cpu().numpy(), *ref, f"shard {h}")
+
+
+def test_decode_step_over_128k_shards_matches_dense():
+    # one new token over the 16 retained shards of 8192 keys (the decode
+    # step's shard partials), merged, against dense attention over 131072 keys
+    cfg = workload.CONFIGS["phase2_128k"]
+    H, S = 16, cfg.Lb
+    q = workload.bf16_normal(cfg.seed * 10 + 5, (1, cfg.Hq, cfg.d))
+    k, v = _shards(H, S, cfg.Hkv, cfg.d, cfg.seed * 10 + 2)
+    o_parts, lse_parts = P.phase2_partial(to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v))
+    o, lse = P.lse_merge(o_parts, lse_parts)
+    torch.cuda.synchronize()
+    ref = attention.dense_attention(f64(q), f64(k).reshape(-1, cfg.Hkv, cfg.d),
+                                    f64(v).reshape(-1, cfg.Hkv, cfg.d), 1 / math.sqrt(cfg.d))
+    check_attention(o.cpu().numpy(), lse.cpu().numpy(), *ref, "decode over 128K")
