@@ -317,17 +317,36 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
 // split space of the shard pass (the larger of the two unmasked passes).
 namespace {
 inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
-int query_parts(int n_shards, int64_t G) { return n_shards + (G > 0 ? 1 : 0) + 1; }
+// Partials of a Phase-2 query step: with the decode kernel (few query rows)
+// every key range of every shard and of the G appended rows is its own
+// partial, so that one merge folds them all; otherwise one per shard, one
+// for the appended rows, and one for the new tokens' own rows.
+struct QueryPlan {
+  bool decode;
+  int np_shard, np_gen;  // key ranges per shard / of the appended rows
+  int parts;
+};
+QueryPlan query_plan(int n_shards, int Tq, int64_t S, int64_t G, int Hq, int Hkv, int d) {
+  QueryPlan p{};
+  p.decode = decode_applies(Tq, Hq, Hkv, d);
+  p.np_shard = p.decode ? decode_parts(n_shards, S, Hkv) : 1;
+  p.np_gen = p.decode && G > 0 ? decode_parts(1, G, Hkv) : 1;
+  p.parts = n_shards * p.np_shard + (G > 0 ? p.np_gen : 0) + 1;
+  return p;
+}
 }  // namespace
 
 size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int64_t G, int Hq,
                                            int Hkv, int d) {
   if (n_shards < 0 || Tq < 0 || S < 0 || G < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1)
     return 0;
-  const size_t parts = (size_t)query_parts(n_shards, G);
+  const QueryPlan plan = query_plan(n_shards, Tq, S, G, Hq, Hkv, d);
+  const size_t parts = (size_t)plan.parts;
   const size_t po = align16(parts * Tq * Hq * d * 4), pl = align16(parts * Hq * Tq * 4);
-  const size_t split = std::max(pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d),
-                                pulsar_phase2_workspace_bytes(1, Tq, G, Hq, Hkv, d));
+  const size_t split =
+      plan.decode ? 0
+                  : std::max(pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d),
+                             pulsar_phase2_workspace_bytes(1, Tq, G, Hq, Hkv, d));
   return po + pl + split;
 }
 
@@ -350,7 +369,8 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
     return PULSAR_EWORKSPACE;
 
-  const int parts = query_parts(n_shards, G);
+  const QueryPlan plan = query_plan(n_shards, Tq, S, G, Hq, Hkv, d);
+  const int parts = plan.parts;
   const int64_t ostride = (int64_t)Tq * Hq * d, lstride = (int64_t)Hq * Tq;
   float* po = static_cast<float*>(workspace);
   float* pl = reinterpret_cast<float*>(static_cast<char*>(workspace) +
@@ -358,13 +378,30 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   char* split = reinterpret_cast<char*>(pl) + align16((size_t)parts * lstride * 4);
   const size_t split_bytes = need - (size_t)(split - static_cast<char*>(workspace));
   int part = 0, st = PULSAR_OK;
-  if (n_shards > 0) {  // parts 0 .. n_shards-1
+  if (plan.decode) {
+    // every key range its own partial: the shards', then the appended rows'
+    if (n_shards > 0) {
+      st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(K),
+                         static_cast<const uint16_t*>(V), n_shards, Tq, S, Hq, Hkv, d,
+                         softmax_scale, po, pl, plan.np_shard, (hipStream_t)stream);
+      if (st != PULSAR_OK) return st;
+      part = n_shards * plan.np_shard;
+    }
+    if (G > 0) {
+      st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(Kg),
+                         static_cast<const uint16_t*>(Vg), 1, Tq, G, Hq, Hkv, d, softmax_scale,
+                         po + part * ostride, pl + part * lstride, plan.np_gen,
+                         (hipStream_t)stream);
+      if (st != PULSAR_OK) return st;
+      part += plan.np_gen;
+    }
+  } else if (n_shards > 0) {  // parts 0 .. n_shards-1
     st = pulsar_phase2_partial(q, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, po, pl, split,
                                split_bytes, stream);
     if (st != PULSAR_OK) return st;
     part = n_shards;
   }
-  if (G > 0) {  // the earlier appended rows, all visible
+  if (!plan.decode && G > 0) {  // the earlier appended rows, all visible
     st = pulsar_phase2_partial(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, po + part * ostride,
                                pl + part * lstride, split, split_bytes, stream);
     if (st != PULSAR_OK) return st;

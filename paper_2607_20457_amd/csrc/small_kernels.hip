@@ -96,11 +96,69 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(
   if (lse && dv == 0) lse[z * (int64_t)Hq * Tq + (int64_t)h * Tq + q] = ell;
 }
 
+// The same merge with one wavefront per output group of four values: lane
+// l folds parts l, l + 64, ..., and the wavefront combines the lanes.  For
+// few outputs and many parts (a decode step: 1024 outputs, tens to hundreds
+// of parts), where a thread per output leaves most of the chip idle and
+// walks the parts one after another.
+__global__ __launch_bounds__(256) void lse_merge_wide_kernel(
+    const float* __restrict__ o_parts, const float* __restrict__ lse_parts, int H, int Tq, int Hq,
+    int d4, int64_t part_ostride, int64_t part_lstride, float* __restrict__ o,
+    float* __restrict__ lse, int64_t total) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= total) return;  // wave-uniform
+  const int dv = (int)(i % d4);
+  int64_t rest = i / d4;
+  const int h = (int)(rest % Hq);
+  rest /= Hq;
+  const int q = (int)(rest % Tq);
+  const int64_t z = rest / Tq;
+
+  const float* lp = lse_parts + z * (int64_t)H * part_lstride + (int64_t)h * Tq + q;
+  float mx = -INFINITY;
+  for (int p = lane; p < H; p += 64) mx = fmaxf(mx, lp[p * part_lstride]);
+  mx = wave_max(mx);
+  const int64_t orow = (((int64_t)q * Hq + h) * d4 + dv);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float ell = -INFINITY;
+  if (mx != -INFINITY) {
+    float sum = 0.f;
+    for (int p = lane; p < H; p += 64) sum += __expf(lp[p * part_lstride] - mx);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, 64);
+    ell = mx + __logf(sum);
+    const f32x4* op = reinterpret_cast<const f32x4*>(o_parts) + z * (int64_t)H * (part_ostride / 4);
+    for (int p = lane; p < H; p += 64) {
+      const float w = __expf(lp[p * part_lstride] - ell);
+      acc += w * op[p * (part_ostride / 4) + orow];
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      acc.x += __shfl_xor(acc.x, off, 64);
+      acc.y += __shfl_xor(acc.y, off, 64);
+      acc.z += __shfl_xor(acc.z, off, 64);
+      acc.w += __shfl_xor(acc.w, off, 64);
+    }
+  }
+  if (lane == 0) {
+    reinterpret_cast<f32x4*>(o)[z * (int64_t)Tq * Hq * d4 + orow] = acc;
+    if (lse && dv == 0) lse[z * (int64_t)Hq * Tq + (int64_t)h * Tq + q] = ell;
+  }
+}
+
 int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz, int Tq, int Hq,
                      int d, int64_t part_ostride, int64_t part_lstride, float* o, float* lse,
                      hipStream_t stream) {
   const int64_t total = (int64_t)nz * Tq * Hq * (d / 4);
   if (total == 0) return PULSAR_OK;
+  if (H >= 8 && total <= 8192) {  // at most 32 workgroups of the per-output form
+    const int64_t blocks = (total + 3) / 4;
+    hipLaunchKernelGGL(lse_merge_wide_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       o_parts, lse_parts, H, Tq, Hq, d / 4, part_ostride, part_lstride, o, lse,
+                       total);
+    return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+  }
   const int64_t blocks = (total + 255) / 256;
   hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, o_parts,
                      lse_parts, H, Tq, Hq, d / 4, part_ostride, part_lstride, o, lse, total);

@@ -158,3 +158,22 @@ def test_decode_step_over_128k_shards_matches_dense():
     ref = attention.dense_attention(f64(q), f64(k).reshape(-1, cfg.Hkv, cfg.d),
                                     f64(v).reshape(-1, cfg.Hkv, cfg.d), 1 / math.sqrt(cfg.d))
     check_attention(o.cpu().numpy(), lse.cpu().numpy(), *ref, "decode over 128K")
+
+
+@pytest.mark.parametrize("H,Tq,Hq,d", [(8, 1, 32, 128), (258, 1, 32, 128), (70, 2, 8, 64)])
+def test_merge_many_parts_few_outputs(H, Tq, Hq, d):
+    # many partials, few outputs: the merge takes one wavefront per output
+    # group, its lanes over the parts; missing parts and large gaps included
+    rng = np.random.default_rng(H + Tq)
+    op = rng.standard_normal((H, Tq, Hq, d)).astype(np.float32)
+    lp = (rng.standard_normal((H, Hq, Tq)) * 30).astype(np.float32)
+    lp[::5] = -np.inf
+    op[::5] = 0
+    lp[:, 0, 0] = -np.inf  # one output with every part missing
+    op[:, 0, 0] = 0
+    o, lse = P.lse_merge(torch.from_numpy(op).cuda(), torch.from_numpy(lp).cuda())
+    torch.cuda.synchronize()
+    ref_o, ref_l = attention.lse_merge(op, lp)
+    np.testing.assert_allclose(o.cpu().numpy(), ref_o, atol=1e-5, rtol=1e-5)
+    np.testing.assert_allclose(lse.cpu().numpy(), ref_l, atol=1e-4, rtol=1e-6)
+    assert np.all(o.cpu().numpy()[0, 0] == 0) and np.isneginf(lse.cpu().numpy()[0, 0])
