@@ -217,7 +217,7 @@ static int phase2_splits(int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d
   const int rows_per_wg = attn_rows_per_wg(group, false);
   const int64_t row_tiles = (Tq + rows_per_wg - 1) / rows_per_wg;
   const int64_t base = row_tiles * (group / heads_per_wg) * Hkv * n_shards;
-  const int64_t target = 512;  // two rounds of 8-wavefront workgroups over 256 CUs
+  const int64_t target = 256;  // one round of 8-wavefront workgroups over 256 CUs
   int64_t ns = (target + base - 1) / base;
   const int64_t max_by_len = (S + 511) / 512;  // keep at least 512 keys per split
   if (ns > max_by_len) ns = max_by_len;
