@@ -170,10 +170,18 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void scorer_kernel(
       for (int q = 0; q < group; ++q) {
         const int4 y = cs[q];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          tf[i] += (uint32_t)((uint32_t)y.x == t[i]) + (uint32_t)((uint32_t)y.y == t[i]) +
-                   (uint32_t)((uint32_t)y.z == t[i]) + (uint32_t)((uint32_t)y.w == t[i]);
+        for (int i = 0; i < 4; ++i) {
+          tf[i] += (uint32_t)((uint32_t)y.x == t[i]);
+          tf[i] += (uint32_t)((uint32_t)y.y == t[i]);
+          tf[i] += (uint32_t)((uint32_t)y.z == t[i]);
+          tf[i] += (uint32_t)((uint32_t)y.w == t[i]);
+        }
       }
+      // The counts stay opaque until here, so that the table index's scaling
+      // is not distributed over the terms: each comparison is then one
+      // compare and one add-with-carry.
+#pragma unroll
+      for (int i = 0; i < 4; ++i) asm volatile("" : "+v"(tf[i]));
       double s = 0.0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
