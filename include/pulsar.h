@@ -261,6 +261,10 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
  * pulsar_phase2_partial), a partial over the G earlier appended rows, an
  * index-causal partial over the Tq new tokens' own rows, and one
  * online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
+ * With few query rows per KV head (Tq * Hq / Hkv <= 32, e.g. a decode
+ * step) one launch computes every key range of the shards and of the
+ * generation shard (token t limited to rows up to G + t) as its own
+ * partial, and one merge follows.
  *
  * q         bf16 [Tq, Hq, d]: the new tokens' queries.
  * Kg, Vg    bf16 [G + Tq, Hkv, d]: the generation shard's appended rows, the

@@ -318,9 +318,10 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
 namespace {
 inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 // Partials of a Phase-2 query step: with the decode kernel (few query rows)
-// every key range of every shard and of the G appended rows is its own
-// partial, so that one merge folds them all; otherwise one per shard, one
-// for the appended rows, and one for the new tokens' own rows.
+// every key range of every shard and of the generation shard (the G
+// appended rows and the new tokens' own) is its own partial, all from one
+// launch, and one merge folds them; otherwise one per shard, one for the
+// appended rows, and one for the new tokens' own rows.
 struct QueryPlan {
   bool decode;
   int np_shard, np_gen;  // key ranges per shard / of the appended rows
@@ -330,8 +331,8 @@ QueryPlan query_plan(int n_shards, int Tq, int64_t S, int64_t G, int Hq, int Hkv
   QueryPlan p{};
   p.decode = decode_applies(Tq, Hq, Hkv, d);
   p.np_shard = p.decode ? decode_parts(n_shards, S, Hkv) : 1;
-  p.np_gen = p.decode && G > 0 ? decode_parts(1, G, Hkv) : 1;
-  p.parts = n_shards * p.np_shard + (G > 0 ? p.np_gen : 0) + 1;
+  p.np_gen = p.decode ? decode_parts(1, G + Tq, Hkv) : 1;
+  p.parts = p.decode ? n_shards * p.np_shard + p.np_gen : n_shards + (G > 0 ? 1 : 0) + 1;
   return p;
 }
 }  // namespace
@@ -379,29 +380,24 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   const size_t split_bytes = need - (size_t)(split - static_cast<char*>(workspace));
   int part = 0, st = PULSAR_OK;
   if (plan.decode) {
-    // every key range its own partial: the shards', then the appended rows'
-    if (n_shards > 0) {
-      st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(K),
-                         static_cast<const uint16_t*>(V), n_shards, Tq, S, Hq, Hkv, d,
-                         softmax_scale, po, pl, plan.np_shard, (hipStream_t)stream);
-      if (st != PULSAR_OK) return st;
-      part = n_shards * plan.np_shard;
-    }
-    if (G > 0) {
-      st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(Kg),
-                         static_cast<const uint16_t*>(Vg), 1, Tq, G, Hq, Hkv, d, softmax_scale,
-                         po + part * ostride, pl + part * lstride, plan.np_gen,
-                         (hipStream_t)stream);
-      if (st != PULSAR_OK) return st;
-      part += plan.np_gen;
-    }
-  } else if (n_shards > 0) {  // parts 0 .. n_shards-1
+    // every key range its own partial, the shards' and then the generation
+    // shard's, in one launch; then one merge
+    const DecodeGen gen{static_cast<const uint16_t*>(Kg), static_cast<const uint16_t*>(Vg), G,
+                        plan.np_gen};
+    st = launch_decode(static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(K),
+                       static_cast<const uint16_t*>(V), n_shards, Tq, S, Hq, Hkv, d,
+                       softmax_scale, po, pl, plan.np_shard, (hipStream_t)stream, &gen);
+    if (st != PULSAR_OK) return st;
+    return launch_lse_merge(po, pl, parts, 1, Tq, Hq, d, ostride, lstride, o, lse,
+                            (hipStream_t)stream);
+  }
+  if (n_shards > 0) {  // parts 0 .. n_shards-1
     st = pulsar_phase2_partial(q, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, po, pl, split,
                                split_bytes, stream);
     if (st != PULSAR_OK) return st;
     part = n_shards;
   }
-  if (!plan.decode && G > 0) {  // the earlier appended rows, all visible
+  if (G > 0) {  // the earlier appended rows, all visible
     st = pulsar_phase2_partial(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, po + part * ostride,
                                pl + part * lstride, split, split_bytes, stream);
     if (st != PULSAR_OK) return st;

@@ -131,9 +131,18 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
 size_t maxidf_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab);
 int decode_parts(int n_shards, int64_t S, int Hkv);
 bool decode_applies(int Tq, int Hq, int Hkv, int d);
+// The generation shard of a decode step, folded into the same launch: rows
+// [0, G) are the tokens appended earlier, row G + t is new token t's own, and
+// token t sees rows 0 .. G + t.
+struct DecodeGen {
+  const uint16_t* K;  // bf16 [G + Tq, Hkv, d]
+  const uint16_t* V;
+  int64_t G;
+  int nparts;         // key ranges (one partial each), after the shards' parts
+};
 int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n_shards, int Tq,
                   int64_t S, int Hq, int Hkv, int d, float scale, float* o, float* lse,
-                  int nparts, hipStream_t stream);
+                  int nparts, hipStream_t stream, const DecodeGen* gen = nullptr);
 int launch_scorer(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
                   int vocab, int scorer, int32_t* sel, float* scores, hipStream_t stream);
 size_t scorer_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab, int scorer);

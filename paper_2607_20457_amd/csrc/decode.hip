@@ -9,8 +9,12 @@
 //
 // Work.  Wave w of a workgroup takes key range `part` of one (shard, KV
 // head) and writes its own (o, lse) partial; the caller merges the parts of
-// a shard (and then the shards) with the log-sum-exp merge.  A wave streams
-// its keys in 32-key steps, on its own (no workgroup barrier):
+// a shard (and then the shards) with the log-sum-exp merge.  In a decode
+// step the generation shard rides in the same launch: workgroups past the
+// shards' take its key ranges, rows [0, G) appended earlier and then the new
+// tokens' own rows, of which token t sees those up to its own (row G + t).
+// A wave streams its keys in 32-key steps, on its own (no workgroup
+// barrier):
 //   K  straight into registers as the A operand of S^T = K Q^T (lane l32
 //      loads key swap_bits23(l32) of the step, so that P comes out in the B
 //      layout of the PV product);
@@ -57,12 +61,18 @@ struct DecodeArgs {
   const uint16_t* K;  // bf16 [n_shards, S, Hkv, D]
   const uint16_t* V;
   int Tq, Hq, Hkv, group;
+  int n_shards;
   int64_t S;
   int nparts;         // key ranges per shard (one wave each)
   int part_len;       // keys per range
+  const uint16_t* Kg; // generation shard, bf16 [G + Tq, Hkv, D] (gen_parts > 0)
+  const uint16_t* Vg;
+  int G;
+  int gen_parts;      // its key ranges (0: no generation shard)
+  int gen_part_len;
   float scale_log2;
-  float* O;           // [n_shards * nparts, Tq, Hq, D]
-  float* lse;         // [n_shards * nparts, Hq, Tq]
+  float* O;           // [n_shards * nparts + gen_parts, Tq, Hq, D]
+  float* lse;         // [n_shards * nparts + gen_parts, Hq, Tq]
 };
 
 template <int D>
@@ -79,28 +89,54 @@ void decode_attn_kernel(DecodeArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31;
   const int g = lane >> 5;
-  // workgroup -> (kv head, shard, group of four parts)
+  // workgroup -> (kv head, shard or generation shard, group of four parts)
   int bid = blockIdx.x;
   const int kvh = bid % a.Hkv;
   bid /= a.Hkv;
   const int pgroups = (a.nparts + DEC_WAVES - 1) / DEC_WAVES;
-  const int shard = bid / pgroups;
-  const int part = (bid % pgroups) * DEC_WAVES + wave;
-  if (part >= a.nparts) return;  // wave-uniform; no barrier follows
-  const int kv_begin = part * a.part_len;
-  const int kv_end = (int)min((int64_t)kv_begin + a.part_len, a.S);
+  const bool gen = bid >= a.n_shards * pgroups;  // workgroup-uniform
+  int part, nparts, part_len;
+  int64_t z, S;
+  const uint16_t *Kz, *Vz;
+  if (!gen) {
+    const int shard = bid / pgroups;
+    part = (bid % pgroups) * DEC_WAVES + wave;
+    nparts = a.nparts;
+    part_len = a.part_len;
+    S = a.S;
+    Kz = a.K + shard * a.S * a.Hkv * D;
+    Vz = a.V + shard * a.S * a.Hkv * D;
+    z = (int64_t)shard * a.nparts + part;
+  } else {
+    part = (bid - a.n_shards * pgroups) * DEC_WAVES + wave;
+    nparts = a.gen_parts;
+    part_len = a.gen_part_len;
+    S = (int64_t)a.G + a.Tq;
+    Kz = a.Kg;
+    Vz = a.Vg;
+    z = (int64_t)a.n_shards * a.nparts + part;
+  }
+  if (part >= nparts) return;  // wave-uniform; no barrier follows
+  const int kv_begin = part * part_len;
+  const int kv_end = (int)min((int64_t)kv_begin + part_len, S);
   const int nsteps = max(0, (kv_end - kv_begin + DEC_KEYS - 1) / DEC_KEYS);
   const int R = a.Tq * a.group;
   const float c2 = a.scale_log2;
+  // Keys from vis_end on weigh zero for this lane's query row: the range's
+  // end, and in the generation shard the rows after the token's own.
+  int vis_end = kv_end;
+  if (gen) vis_end = min(vis_end, a.G + l32 / a.group + 1);
+  // a step whose keys all lie below mask_from needs no mask in any lane
+  const int mask_from = gen ? min(kv_end, a.G + 1) : kv_end;
 
   // K/V of this shard through buffer resources, 32-bit byte offsets.
-  const int64_t zstride = a.S * a.Hkv * D;
+  const int64_t zstride = S * a.Hkv * D;
   const uint32_t row_bytes = (uint32_t)(a.Hkv * D * 2);
   const uint32_t head_off = (uint32_t)(kvh * D * 2);
   const __amdgpu_buffer_rsrc_t k_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.K + shard * zstride), (short)0, (int)(zstride * 2), kDecBufferFlags);
+      const_cast<uint16_t*>(Kz), (short)0, (int)(zstride * 2), kDecBufferFlags);
   const __amdgpu_buffer_rsrc_t v_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(a.V + shard * zstride), (short)0, (int)(zstride * 2), kDecBufferFlags);
+      const_cast<uint16_t*>(Vz), (short)0, (int)(zstride * 2), kDecBufferFlags);
 
   // ---- Q fragments (B operand): column l32 = packed row (token, head) ----
   bf16x8 qf[DS];
@@ -195,22 +231,26 @@ void decode_attn_kernel(DecodeArgs a) {
       load_k(j + 1, kbuf[KB ^ 1]);
       issue_v(j + 1, KB ^ 1);
     }
-    // keys past the range end weigh zero; lane (l32, g) holds rows
+    // keys from vis_end on weigh zero; lane (l32, g) holds rows
     // 8(v/4) + 4g + v%4, i.e. keys swap23 of those
     const int k0 = kv_begin + j * DEC_KEYS;
-    if (k0 + DEC_KEYS > kv_end) {
+    if (k0 + DEC_KEYS > mask_from) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = 8 * (v >> 2) + 4 * g + (v & 3);
-        if (k0 + swap23(row) >= kv_end) S[v] = -INFINITY;
+        if (k0 + swap23(row) >= vis_end) S[v] = -INFINITY;
       }
     }
     float mx = S[0];
 #pragma unroll
     for (int v = 1; v < 16; ++v) mx = fmaxf(mx, S[v]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
-    const float m_new = fmaxf(m_run, mx);  // finite: the step's first key is in range
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    // A row may have seen no key yet (a generation-shard range that starts
+    // after its token's own row): its maximum stays -inf, and the weights
+    // are taken against 0 so that they come out 0 rather than NaN.
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
 #pragma unroll
     for (int e = 0; e < DT; ++e) acc[e] *= alpha;
     l_run *= alpha;
@@ -222,7 +262,7 @@ void decode_attn_kernel(DecodeArgs a) {
       f32x8 p;
 #pragma unroll
       for (int v = 0; v < 8; ++v) {
-        p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[8 * c + v], c2, -m_new));
+        p[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(S[8 * c + v], c2, -m_use));
         l_run += p[v];
       }
       P[c] = __builtin_convertvector(p, bf16x8);
@@ -254,7 +294,6 @@ void decode_attn_kernel(DecodeArgs a) {
   if (r < R) {
     const int tok = r / a.group;
     const int head = kvh * a.group + (r - tok * a.group);
-    const int64_t z = (int64_t)shard * a.nparts + part;
     float* o = a.O + z * (int64_t)a.Tq * a.Hq * D + ((int64_t)tok * a.Hq + head) * D;
 #pragma unroll
     for (int e = 0; e < DT; ++e)
@@ -276,7 +315,7 @@ void decode_attn_kernel(DecodeArgs a) {
 // Key ranges per shard for the decode kernel: enough waves for two
 // four-wave workgroups per compute unit, at least 256 keys per range.
 int decode_parts(int n_shards, int64_t S, int Hkv) {
-  if (S <= 0) return 1;
+  if (S <= 0 || n_shards <= 0 || Hkv <= 0) return 1;
   const int64_t waves = (int64_t)n_shards * Hkv;
   int64_t np = (256 * 8 + waves - 1) / waves;
   const int64_t max_by_len = (S + 255) / 256;
@@ -292,7 +331,7 @@ bool decode_applies(int Tq, int Hq, int Hkv, int d) {
 
 int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n_shards, int Tq,
                   int64_t S, int Hq, int Hkv, int d, float scale, float* o, float* lse,
-                  int nparts, hipStream_t stream) {
+                  int nparts, hipStream_t stream, const DecodeGen* gen) {
   DecodeArgs a{};
   a.Q = q;
   a.K = K;
@@ -301,13 +340,24 @@ int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.group = Hq / Hkv;
+  a.n_shards = n_shards;
   a.S = S;
   a.nparts = nparts;
   a.part_len = (int)((S + nparts - 1) / nparts);
+  if (gen != nullptr && gen->nparts > 0) {
+    const int64_t rows = gen->G + Tq;
+    a.Kg = gen->K;
+    a.Vg = gen->V;
+    a.G = (int)gen->G;
+    a.gen_parts = gen->nparts;
+    a.gen_part_len = (int)((rows + gen->nparts - 1) / gen->nparts);
+  }
   a.scale_log2 = scale * 1.4426950408889634f;
   a.O = o;
   a.lse = lse;
-  const int64_t nwg = (int64_t)n_shards * Hkv * ((nparts + DEC_WAVES - 1) / DEC_WAVES);
+  const int64_t pgroups = (nparts + DEC_WAVES - 1) / DEC_WAVES;
+  const int64_t nwg =
+      (int64_t)Hkv * ((int64_t)n_shards * pgroups + (a.gen_parts + DEC_WAVES - 1) / DEC_WAVES);
   if (nwg == 0) return PULSAR_OK;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const size_t lds = (size_t)DEC_WAVES * 2 * DEC_KEYS * d * 2;  // two V stages per wave

@@ -178,6 +178,9 @@ def test_phase2_query_validation():
     assert call(ws=None) == EWS
     assert call(wsb=ws_need - 1) == EWS
     assert call(Tq=0) == 0
+    # no retained shards but a nonzero shard length: sized without dividing by zero
+    assert lib.pulsar_phase2_query_workspace_bytes(0, 1, 512, 3, 32, 8, 128) > 0
+    assert lib.pulsar_phase2_workspace_bytes(0, 1, 512, 32, 8, 128) == 0
 
 
 def test_chunk_summaries_validation():

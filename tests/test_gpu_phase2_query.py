@@ -22,6 +22,7 @@ pytestmark = pytest.mark.gpu
 def _run_and_check(q, kg, vg, G, k=None, v=None, what=""):
     d = q.shape[-1]
     scale = 1.0 / math.sqrt(d)
+    print(f"phase2_query parity: {what}", flush=True)
     o, lse = P.phase2_query(to_dev_bf16(q), to_dev_bf16(kg), to_dev_bf16(vg), G,
                             None if k is None else to_dev_bf16(k),
                             None if v is None else to_dev_bf16(v))
@@ -80,3 +81,23 @@ def test_peaked_queries():
     k = workload.bf16_normal(703, (8, 1024, 8, 128))
     v = workload.bf16_normal(704, (8, 1024, 8, 128))
     _run_and_check(q, kg, vg, 9, k, v, "peaked")
+
+
+@pytest.mark.parametrize("Hq,Hkv,d,Tq,G,ns,S", [
+    (32, 8, 128, 8, 5, 3, 700),      # 32 packed rows: the decode kernel, causal new rows
+    (8, 8, 128, 32, 0, 0, 0),        # one head per KV head, new tokens only
+    (16, 8, 64, 16, 600, 2, 300),    # generation shard in three key ranges
+    (32, 8, 128, 3, 2000, 4, 512),   # eight generation ranges, the last holding the new rows
+    (4, 1, 64, 7, 0, 1, 100),        # one KV head
+])
+def test_few_rows_one_launch(Hq, Hkv, d, Tq, G, ns, S):
+    # Tq * Hq / Hkv <= 32: shards and generation shard in one decode launch,
+    # token t limited to generation rows up to G + t
+    seed = 900 + Hq + Tq + G
+    q = workload.bf16_normal(seed, (Tq, Hq, d))
+    kg = workload.bf16_normal(seed + 1, (G + Tq, Hkv, d))
+    vg = workload.bf16_normal(seed + 2, (G + Tq, Hkv, d))
+    k = workload.bf16_normal(seed + 3, (ns, S, Hkv, d)) if ns else None
+    v = workload.bf16_normal(seed + 4, (ns, S, Hkv, d)) if ns else None
+    _run_and_check(q, kg, vg, G, k, v, f"few rows Hq={Hq} Hkv={Hkv} d={d} Tq={Tq} G={G} "
+                   f"shards={ns}x{S}")
