@@ -280,7 +280,8 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
  * EINVAL: negative sizes, Hq % Hkv != 0, NULL required pointers, misaligned
  *         buffers, scale not finite and > 0.  EWORKSPACE: workspace NULL,
  *         misaligned or too small.
- * EUNSUPPORTED: d not in {64, 128}; Hq / Hkv not 1, 2 or a multiple of 4.
+ * EUNSUPPORTED: d not in {64, 128}; Hq / Hkv not 1, 2 or a multiple of 4;
+ *         one shard's or the generation shard's K at 2 GiB or more.
  */
 size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int64_t G, int Hq,
                                            int Hkv, int d);

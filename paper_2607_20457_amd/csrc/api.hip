@@ -317,23 +317,62 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
 // split space of the shard pass (the larger of the two unmasked passes).
 namespace {
 inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
-// Partials of a Phase-2 query step: with the decode kernel (few query rows)
-// every key range of every shard and of the generation shard (the G
-// appended rows and the new tokens' own) is its own partial, all from one
-// launch, and one merge folds them; otherwise one per shard, one for the
-// appended rows, and one for the new tokens' own rows.
+// Partials of a Phase-2 query step; every key range is its own partial and
+// one merge folds them all.  With the decode kernel (few query rows) one
+// launch covers the ranges of every shard and of the generation shard (the
+// G appended rows and the new tokens' own).  Otherwise the attention kernel
+// gives the key splits of the shards, then those of the G appended rows, and
+// one index-causal partial over the new tokens' own rows.
 struct QueryPlan {
   bool decode;
-  int np_shard, np_gen;  // key ranges per shard / of the appended rows
+  int np_shard, np_gen;  // key ranges per shard / of the generation shard's rows
   int parts;
 };
 QueryPlan query_plan(int n_shards, int Tq, int64_t S, int64_t G, int Hq, int Hkv, int d) {
   QueryPlan p{};
   p.decode = decode_applies(Tq, Hq, Hkv, d);
-  p.np_shard = p.decode ? decode_parts(n_shards, S, Hkv) : 1;
-  p.np_gen = p.decode ? decode_parts(1, G + Tq, Hkv) : 1;
-  p.parts = p.decode ? n_shards * p.np_shard + p.np_gen : n_shards + (G > 0 ? 1 : 0) + 1;
+  if (p.decode) {
+    p.np_shard = decode_parts(n_shards, S, Hkv);
+    p.np_gen = decode_parts(1, G + Tq, Hkv);
+    p.parts = n_shards * p.np_shard + p.np_gen;
+  } else {
+    p.np_shard = n_shards > 0 ? phase2_splits(n_shards, Tq, S, Hq, Hkv, d) : 0;
+    p.np_gen = G > 0 ? phase2_splits(1, Tq, G, Hq, Hkv, d) : 0;
+    p.parts = n_shards * p.np_shard + p.np_gen + 1;
+  }
   return p;
+}
+
+// Unmasked attention of the Tq queries over nz key sets of S rows each, every
+// one cut into ns key splits; split s of set z writes partial z * ns + s.
+int launch_split_parts(const void* q, const void* K, const void* V, int nz, int Tq, int64_t S,
+                       int Hq, int Hkv, int d, float scale, int ns, float* po, float* pl,
+                       hipStream_t stream) {
+  AttnLaunch a{};
+  a.Q = static_cast<const uint16_t*>(q);
+  a.K = static_cast<const uint16_t*>(K);
+  a.V = static_cast<const uint16_t*>(V);
+  a.q_zstride = 0;
+  a.kv_zstride = S * Hkv * d;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.d = d;
+  a.n_q = Tq;
+  a.n_kv = (int)S;
+  a.causal = 0;
+  a.nsplit = ns;
+  a.split_len = (int)((S + ns - 1) / ns);
+  a.nz_kv = nz;
+  a.map = RowMap{};
+  a.map.mode = MAP_IDENTITY;
+  a.sel = nullptr;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.o_bf16 = 0;
+  a.o_zstride = (int64_t)Tq * Hq * d;
+  a.lse_zstride = (int64_t)Hq * Tq;
+  a.O = po;
+  a.lse = pl;
+  return launch_attention(a, stream);
 }
 }  // namespace
 
@@ -343,12 +382,7 @@ size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int6
     return 0;
   const QueryPlan plan = query_plan(n_shards, Tq, S, G, Hq, Hkv, d);
   const size_t parts = (size_t)plan.parts;
-  const size_t po = align16(parts * Tq * Hq * d * 4), pl = align16(parts * Hq * Tq * 4);
-  const size_t split =
-      plan.decode ? 0
-                  : std::max(pulsar_phase2_workspace_bytes(n_shards, Tq, S, Hq, Hkv, d),
-                             pulsar_phase2_workspace_bytes(1, Tq, G, Hq, Hkv, d));
-  return po + pl + split;
+  return align16(parts * Tq * Hq * d * 4) + align16(parts * Hq * Tq * 4);
 }
 
 int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
@@ -362,6 +396,8 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   if (!heads_supported(Hq, Hkv)) return PULSAR_EUNSUPPORTED;
   if (G + Tq >= PULSAR_MAX_ROWS || (G + Tq) * Hkv * d * 2 >= ((int64_t)1 << 31))
     return PULSAR_EUNSUPPORTED;
+  if (S * Hkv * d * 2 >= ((int64_t)1 << 31) || Tq >= PULSAR_MAX_ROWS)
+    return PULSAR_EUNSUPPORTED;  // byte offsets within a shard must fit 32 bits
   if (Tq == 0) return PULSAR_OK;
   if (q == nullptr || Kg == nullptr || Vg == nullptr || o == nullptr) return PULSAR_EINVAL;
   if (n_shards > 0 && S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;
@@ -376,8 +412,6 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   float* po = static_cast<float*>(workspace);
   float* pl = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                        align16((size_t)parts * ostride * 4));
-  char* split = reinterpret_cast<char*>(pl) + align16((size_t)parts * lstride * 4);
-  const size_t split_bytes = need - (size_t)(split - static_cast<char*>(workspace));
   int part = 0, st = PULSAR_OK;
   if (plan.decode) {
     // every key range its own partial, the shards' and then the generation
@@ -391,17 +425,17 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
     return launch_lse_merge(po, pl, parts, 1, Tq, Hq, d, ostride, lstride, o, lse,
                             (hipStream_t)stream);
   }
-  if (n_shards > 0) {  // parts 0 .. n_shards-1
-    st = pulsar_phase2_partial(q, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, po, pl, split,
-                               split_bytes, stream);
+  if (n_shards > 0) {  // the shards' key splits
+    st = launch_split_parts(q, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, plan.np_shard,
+                            po, pl, (hipStream_t)stream);
     if (st != PULSAR_OK) return st;
-    part = n_shards;
+    part = n_shards * plan.np_shard;
   }
-  if (G > 0) {  // the earlier appended rows, all visible
-    st = pulsar_phase2_partial(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, po + part * ostride,
-                               pl + part * lstride, split, split_bytes, stream);
+  if (G > 0) {  // the earlier appended rows, all visible, in key splits
+    st = launch_split_parts(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, plan.np_gen,
+                            po + part * ostride, pl + part * lstride, (hipStream_t)stream);
     if (st != PULSAR_OK) return st;
-    ++part;
+    part += plan.np_gen;
   }
   // the new tokens' own rows: index-causal, square
   const int64_t row = (int64_t)Hkv * d;

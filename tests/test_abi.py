@@ -175,6 +175,7 @@ def test_phase2_query_validation():
     assert call(o=None) == EINVAL
     assert call(q=FAKE + 4) == EINVAL      # misaligned
     assert call(d=96) == EUNSUP
+    assert call(S=1 << 21) == EUNSUP       # a shard past 2 GiB of K
     assert call(ws=None) == EWS
     assert call(wsb=ws_need - 1) == EWS
     assert call(Tq=0) == 0
