@@ -9,7 +9,8 @@
 // turned by the angle p * w_i.
 //
 // Thread (row, j) owns pairs 8j .. 8j+7 of every head of its row: 16-byte
-// loads of x[8j .. 8j+7] and x[d/2+8j .. d/2+8j+7].  Its eight angles are
+// loads of x[8j .. 8j+7] and x[d/2+8j .. d/2+8j+7], four heads at a time
+// with the next four in flight.  Its eight angles are
 // formed once, in fp64 (p * w_i, then reduced to [-pi, pi] with a two-part
 // 2*pi), and their sine and cosine (fp32, on the reduced angle) serve every
 // head of the row.  The rotation is evaluated in fp32 and rounded once to
@@ -35,28 +36,54 @@ constexpr double kTwoPiHi = 6.283185307179586;
 constexpr double kTwoPiLo = 2.4492935982947064e-16;
 constexpr double kInvTwoPi = 0.15915494309189535;
 
-template <int D>
+template <int D, bool HAS_POS>
 __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict__ X,
                                                             int64_t rows, int64_t n_rows, int H,
                                                             const int32_t* __restrict__ pos,
                                                             int64_t pos_offset, RopeFreqs f) {
   constexpr int G = D / 16;  // threads per row
+  constexpr int U = 4;       // heads per batch of loads
   const int64_t t = (int64_t)blockIdx.x * kRopeThreads + threadIdx.x;
   const int64_t row = t / G;
   const int j = (int)(t % G);
   if (row >= rows) return;
-  const int64_t p = (pos ? (int64_t)pos[row] : row % n_rows) + pos_offset;
+  uint16_t* base = X + row * (int64_t)H * D + 8 * j;
+  // Heads go U at a time.  The first batch is loaded before anything else,
+  // so that it travels while the angles are formed, and each later batch is
+  // loaded before the one in hand is rotated and stored.
+  u32x4 lo[U], hi[U];
+  // branch-free, so that the compiler can count the loads in flight: a head
+  // past the last one re-reads the last (it is never stored)
+  auto load = [&](int h0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int hh = min(h0 + u, H - 1);
+      lo[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D);
+      hi[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D + D / 2);
+    }
+  };
+  // The eight frequencies and the position are requested first and the
+  // first batch of data after them: memory counters retire in order, so
+  // waiting for the frequencies then leaves the data in flight.
+  double w[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) w[v] = f.w[8 * j + v];
+  int64_t p = HAS_POS ? (int64_t)pos[row] : row % n_rows;
+  load(0);
+#pragma unroll
+  for (int v = 0; v < 8; ++v) asm volatile("" : "+v"(w[v]));
+  asm volatile("" : "+v"(p));
+  p += pos_offset;
   const double pd = (double)p;
   float c[8], s[8];
 #pragma unroll
   for (int v = 0; v < 8; ++v) {
-    const double a = pd * f.w[8 * j + v];
+    const double a = pd * w[v];
     const double k = rint(a * kInvTwoPi);
     double r = fma(-k, kTwoPiHi, a);
     r = fma(-k, kTwoPiLo, r);
     sincosf((float)r, &s[v], &c[v]);
   }
-  uint16_t* base = X + row * (int64_t)H * D + 8 * j;
   auto rotate = [&](const u32x4 lo, const u32x4 hi, u32x4& olo, u32x4& ohi) {
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -72,31 +99,22 @@ __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict
       ohi[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(yhi, bf16x2));
     }
   };
-  // four heads at a time: all eight loads in flight before the first store
-  constexpr int U = 4;
-  int h = 0;
-  for (; h + U <= H; h += U) {
-    u32x4 lo[U], hi[U];
+  for (int h = 0; h < H; h += U) {
+    u32x4 clo[U], chi[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      lo[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)(h + u) * D);
-      hi[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)(h + u) * D + D / 2);
+      clo[u] = lo[u];
+      chi[u] = hi[u];
     }
+    if (h + U < H) load(h + U);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      u32x4 olo, ohi;
-      rotate(lo[u], hi[u], olo, ohi);
-      *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D) = olo;
-      *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D + D / 2) = ohi;
-    }
-  }
-  for (; h < H; ++h) {
-    u32x4* plo = reinterpret_cast<u32x4*>(base + (int64_t)h * D);
-    u32x4* phi = reinterpret_cast<u32x4*>(base + (int64_t)h * D + D / 2);
-    u32x4 olo, ohi;
-    rotate(*plo, *phi, olo, ohi);
-    *plo = olo;
-    *phi = ohi;
+    for (int u = 0; u < U; ++u)
+      if (h + u < H) {
+        u32x4 olo, ohi;
+        rotate(clo[u], chi[u], olo, ohi);
+        *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D) = olo;
+        *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D + D / 2) = ohi;
+      }
   }
 }
 
@@ -126,12 +144,10 @@ int pulsar_rope(void* X, int batch, int64_t n_rows, int H, int d, const int32_t*
   const int64_t blocks = (threads + kRopeThreads - 1) / kRopeThreads;
   if (blocks > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   auto s = (hipStream_t)stream;
-  if (d == 128)
-    hipLaunchKernelGGL(rope_kernel<128>, dim3((unsigned)blocks), dim3(kRopeThreads), 0, s,
-                       (uint16_t*)X, rows, n_rows, H, pos, pos_offset, f);
-  else
-    hipLaunchKernelGGL(rope_kernel<64>, dim3((unsigned)blocks), dim3(kRopeThreads), 0, s,
-                       (uint16_t*)X, rows, n_rows, H, pos, pos_offset, f);
+  const auto kern = d == 128 ? (pos ? rope_kernel<128, true> : rope_kernel<128, false>)
+                             : (pos ? rope_kernel<64, true> : rope_kernel<64, false>);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kRopeThreads), 0, s, (uint16_t*)X, rows,
+                     n_rows, H, pos, pos_offset, f);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
 
