@@ -59,9 +59,12 @@ int launch_copy_rows(const void* src, int64_t src_pitch, void* dst, int64_t dst_
 
 // ---------------------------------------------------------------------------
 // Online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
-// Thread = four consecutive head_dim entries of one (z, query, head).
-// l = m + ln sum_h exp(l_h - m) with m = max_h l_h, then
-// o = sum_h exp(l_h - l) o_h; -inf partials weigh zero.
+// Thread = four consecutive head_dim entries of one (z, query, head).  One
+// pass over the parts, eight at a time with all their loads issued
+// together: the running maximum m, s = sum_h exp(l_h - m) and
+// a = sum_h exp(l_h - m) o_h are rescaled when m rises; then l = m + ln s and
+// o = a / s.  -inf partials weigh zero.
+constexpr int kMergeChunk = 8;
 __global__ __launch_bounds__(256) void lse_merge_kernel(
     const float* __restrict__ o_parts, const float* __restrict__ lse_parts, int H, int Tq, int Hq,
     int d4, int64_t part_ostride, int64_t part_lstride, float* __restrict__ o,
@@ -76,21 +79,43 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(
   const int64_t z = rest / Tq;
 
   const float* lp = lse_parts + z * (int64_t)H * part_lstride + (int64_t)h * Tq + q;
-  float mx = -INFINITY;
-  for (int p = 0; p < H; ++p) mx = fmaxf(mx, lp[p * part_lstride]);
   const int64_t orow = (((int64_t)q * Hq + h) * d4 + dv);
+  const f32x4* op = reinterpret_cast<const f32x4*>(o_parts) + z * (int64_t)H * (part_ostride / 4);
+  float m = -INFINITY, sum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float ell = -INFINITY;
-  if (mx != -INFINITY) {
-    float sum = 0.f;
-    for (int p = 0; p < H; ++p) sum += __expf(lp[p * part_lstride] - mx);
-    ell = mx + __logf(sum);
-    const f32x4* op = reinterpret_cast<const f32x4*>(o_parts) + z * (int64_t)H * (part_ostride / 4);
-    for (int p = 0; p < H; ++p) {
-      const float w = __expf(lp[p * part_lstride] - ell);
-      const f32x4 v = op[p * (part_ostride / 4) + orow];
-      acc += w * v;
+  for (int p0 = 0; p0 < H; p0 += kMergeChunk) {
+    float l[kMergeChunk];
+    f32x4 v[kMergeChunk];
+#pragma unroll
+    for (int u = 0; u < kMergeChunk; ++u) {
+      const int p = min(p0 + u, H - 1);  // a part past the last re-reads it, weighing zero
+      l[u] = lp[p * part_lstride];
+      v[u] = op[p * (part_ostride / 4) + orow];
     }
+    float cm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kMergeChunk; ++u)
+      if (p0 + u < H) cm = fmaxf(cm, l[u]);
+    // branch-free, so that all sixteen loads are issued before the first
+    // wait; with no finite partial yet the weights are taken against 0 and
+    // come out 0
+    const float nm = fmaxf(m, cm);
+    const float nm_use = nm == -INFINITY ? 0.f : nm;
+    const float alpha = __expf(m - nm_use);  // 0 while m is -inf
+    sum *= alpha;
+    acc *= alpha;
+#pragma unroll
+    for (int u = 0; u < kMergeChunk; ++u) {
+      const float w = p0 + u < H ? __expf(l[u] - nm_use) : 0.f;
+      sum += w;
+      acc += w * v[u];
+    }
+    m = nm;
+  }
+  float ell = -INFINITY;
+  if (m != -INFINITY) {
+    ell = m + __logf(sum);
+    acc *= 1.f / sum;
   }
   reinterpret_cast<f32x4*>(o)[z * (int64_t)Tq * Hq * d4 + orow] = acc;
   if (lse && dv == 0) lse[z * (int64_t)Hq * Tq + (int64_t)h * Tq + q] = ell;
