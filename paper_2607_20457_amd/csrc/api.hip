@@ -321,22 +321,31 @@ inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 // one merge folds them all.  With the decode kernel (few query rows) one
 // launch covers the ranges of every shard and of the generation shard (the
 // G appended rows and the new tokens' own).  Otherwise the attention kernel
-// gives the key splits of the shards, then those of the G appended rows, and
-// one index-causal partial over the new tokens' own rows.
+// gives the key splits of the shards; a generation shard of at most
+// kGenDecodeRows rows then goes to the decode kernel in 32-row tiles (each
+// token limited to the rows up to its own), and a longer one to the
+// attention kernel: key splits of the G appended rows, and one index-causal
+// partial over the new tokens' own rows.
+constexpr int64_t kGenDecodeRows = 4096;
 struct QueryPlan {
-  bool decode;
+  bool decode;      // everything in one decode launch
+  bool gen_decode;  // the generation shard in a decode launch
   int np_shard, np_gen;  // key ranges per shard / of the generation shard's rows
   int parts;
 };
 QueryPlan query_plan(int n_shards, int Tq, int64_t S, int64_t G, int Hq, int Hkv, int d) {
   QueryPlan p{};
   p.decode = decode_applies(Tq, Hq, Hkv, d);
+  p.gen_decode = p.decode || ((d == 64 || d == 128) && Hq / Hkv <= 32 && G + Tq <= kGenDecodeRows);
   if (p.decode) {
     p.np_shard = decode_parts(n_shards, S, Hkv);
+  } else {
+    p.np_shard = n_shards > 0 ? phase2_splits(n_shards, Tq, S, Hq, Hkv, d) : 0;
+  }
+  if (p.gen_decode) {
     p.np_gen = decode_parts(1, G + Tq, Hkv);
     p.parts = n_shards * p.np_shard + p.np_gen;
   } else {
-    p.np_shard = n_shards > 0 ? phase2_splits(n_shards, Tq, S, Hq, Hkv, d) : 0;
     p.np_gen = G > 0 ? phase2_splits(1, Tq, G, Hq, Hkv, d) : 0;
     p.parts = n_shards * p.np_shard + p.np_gen + 1;
   }
@@ -430,6 +439,16 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
                             po, pl, (hipStream_t)stream);
     if (st != PULSAR_OK) return st;
     part = n_shards * plan.np_shard;
+  }
+  if (plan.gen_decode) {  // the generation shard's rows, each token up to its own
+    const DecodeGen gen{static_cast<const uint16_t*>(Kg), static_cast<const uint16_t*>(Vg), G,
+                        plan.np_gen};
+    st = launch_decode(static_cast<const uint16_t*>(q), nullptr, nullptr, 0, Tq, 0, Hq, Hkv, d,
+                       softmax_scale, po + part * ostride, pl + part * lstride, 1,
+                       (hipStream_t)stream, &gen);
+    if (st != PULSAR_OK) return st;
+    return launch_lse_merge(po, pl, parts, 1, Tq, Hq, d, ostride, lstride, o, lse,
+                            (hipStream_t)stream);
   }
   if (G > 0) {  // the earlier appended rows, all visible, in key splits
     st = launch_split_parts(q, Kg, Vg, 1, Tq, G, Hq, Hkv, d, softmax_scale, plan.np_gen,

@@ -4,11 +4,12 @@
 // token (or a few) attends to every shard: the work is bound by streaming
 // K/V from HBM, and the query rows are too few for the Phase-1 tiles.
 //
-// Rows.  The R = Tq * group query rows that read one KV head (token t, head
-// kvh*group + h -> row t*group + h) form one 32-row tile, R <= 32.
+// Rows.  The query rows that read one KV head (token t, head kvh*group + h
+// -> row t*group + h) form 32-row tiles of 32 / group tokens each; a decode
+// step has one tile.
 //
 // Work.  Wave w of a workgroup takes key range `part` of one (shard, KV
-// head) and writes its own (o, lse) partial; the caller merges the parts of
+// head) for one row tile and writes its own (o, lse) partial; the caller merges the parts of
 // a shard (and then the shards) with the log-sum-exp merge.  In a decode
 // step the generation shard rides in the same launch: workgroups past the
 // shards' take its key ranges, rows [0, G) appended earlier and then the new
@@ -70,6 +71,8 @@ struct DecodeArgs {
   int G;
   int gen_parts;      // its key ranges (0: no generation shard)
   int gen_part_len;
+  int tile_tokens;    // tokens per 32-row tile, 32 / group
+  int row_tiles;      // tiles over the Tq tokens
   float scale_log2;
   float* O;           // [n_shards * nparts + gen_parts, Tq, Hq, D]
   float* lse;         // [n_shards * nparts + gen_parts, Hq, Tq]
@@ -93,41 +96,48 @@ void decode_attn_kernel(DecodeArgs a) {
   int bid = blockIdx.x;
   const int kvh = bid % a.Hkv;
   bid /= a.Hkv;
-  const int pgroups = (a.nparts + DEC_WAVES - 1) / DEC_WAVES;
+  // wave index within a (shard, KV head): key range wi / row_tiles, row
+  // tile wi % row_tiles (the waves of a workgroup share key ranges)
+  const int pgroups = (a.nparts * a.row_tiles + DEC_WAVES - 1) / DEC_WAVES;
   const bool gen = bid >= a.n_shards * pgroups;  // workgroup-uniform
-  int part, nparts, part_len;
-  int64_t z, S;
+  int wi, nparts, part_len;
+  int64_t S;
   const uint16_t *Kz, *Vz;
+  int shard = 0;
   if (!gen) {
-    const int shard = bid / pgroups;
-    part = (bid % pgroups) * DEC_WAVES + wave;
+    shard = bid / pgroups;
+    wi = (bid % pgroups) * DEC_WAVES + wave;
     nparts = a.nparts;
     part_len = a.part_len;
     S = a.S;
     Kz = a.K + shard * a.S * a.Hkv * D;
     Vz = a.V + shard * a.S * a.Hkv * D;
-    z = (int64_t)shard * a.nparts + part;
   } else {
-    part = (bid - a.n_shards * pgroups) * DEC_WAVES + wave;
+    wi = (bid - a.n_shards * pgroups) * DEC_WAVES + wave;
     nparts = a.gen_parts;
     part_len = a.gen_part_len;
     S = (int64_t)a.G + a.Tq;
     Kz = a.Kg;
     Vz = a.Vg;
-    z = (int64_t)a.n_shards * a.nparts + part;
   }
+  const int part = wi / a.row_tiles, tile = wi - part * a.row_tiles;
   if (part >= nparts) return;  // wave-uniform; no barrier follows
+  // partial of this key range; each row tile writes its own tokens' rows of it
+  const int64_t z = (gen ? (int64_t)a.n_shards * a.nparts : (int64_t)shard * a.nparts) + part;
+  const int tok0 = tile * a.tile_tokens;
+  const int R = min(a.tile_tokens, a.Tq - tok0) * a.group;  // live rows of the tile
   const int kv_begin = part * part_len;
-  const int kv_end = (int)min((int64_t)kv_begin + part_len, S);
+  int kv_end = (int)min((int64_t)kv_begin + part_len, S);
+  // in the generation shard no row of the tile sees past its last token's own
+  if (gen) kv_end = min(kv_end, a.G + tok0 + R / a.group);
   const int nsteps = max(0, (kv_end - kv_begin + DEC_KEYS - 1) / DEC_KEYS);
-  const int R = a.Tq * a.group;
   const float c2 = a.scale_log2;
   // Keys from vis_end on weigh zero for this lane's query row: the range's
   // end, and in the generation shard the rows after the token's own.
   int vis_end = kv_end;
-  if (gen) vis_end = min(vis_end, a.G + l32 / a.group + 1);
+  if (gen) vis_end = min(vis_end, a.G + tok0 + l32 / a.group + 1);
   // a step whose keys all lie below mask_from needs no mask in any lane
-  const int mask_from = gen ? min(kv_end, a.G + 1) : kv_end;
+  const int mask_from = gen ? min(kv_end, a.G + tok0 + 1) : kv_end;
 
   // K/V of this shard through buffer resources, 32-bit byte offsets.
   const int64_t zstride = S * a.Hkv * D;
@@ -142,8 +152,9 @@ void decode_attn_kernel(DecodeArgs a) {
   bf16x8 qf[DS];
   {
     const int r = l32;
-    const int tok = r / a.group;
-    const int head = kvh * a.group + (r - tok * a.group);
+    const int tl = r / a.group;
+    const int tok = tok0 + tl;
+    const int head = kvh * a.group + (r - tl * a.group);
     const bf16x8* src =
         reinterpret_cast<const bf16x8*>(a.Q + ((int64_t)tok * a.Hq + head) * D) + g;
 #pragma unroll
@@ -292,8 +303,9 @@ void decode_attn_kernel(DecodeArgs a) {
   const float inv = lr_tot > 0.f ? 1.f / lr_tot : 0.f;
   const int r = l32;
   if (r < R) {
-    const int tok = r / a.group;
-    const int head = kvh * a.group + (r - tok * a.group);
+    const int tl = r / a.group;
+    const int tok = tok0 + tl;
+    const int head = kvh * a.group + (r - tl * a.group);
     float* o = a.O + z * (int64_t)a.Tq * a.Hq * D + ((int64_t)tok * a.Hq + head) * D;
 #pragma unroll
     for (int e = 0; e < DT; ++e)
@@ -344,6 +356,9 @@ int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n
   a.S = S;
   a.nparts = nparts;
   a.part_len = (int)((S + nparts - 1) / nparts);
+  a.tile_tokens = 32 / a.group;
+  if (a.tile_tokens < 1) return PULSAR_EUNSUPPORTED;
+  a.row_tiles = (Tq + a.tile_tokens - 1) / a.tile_tokens;
   if (gen != nullptr && gen->nparts > 0) {
     const int64_t rows = gen->G + Tq;
     a.Kg = gen->K;
@@ -355,9 +370,10 @@ int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n
   a.scale_log2 = scale * 1.4426950408889634f;
   a.O = o;
   a.lse = lse;
-  const int64_t pgroups = (nparts + DEC_WAVES - 1) / DEC_WAVES;
+  const int64_t pgroups = ((int64_t)nparts * a.row_tiles + DEC_WAVES - 1) / DEC_WAVES;
   const int64_t nwg =
-      (int64_t)Hkv * ((int64_t)n_shards * pgroups + (a.gen_parts + DEC_WAVES - 1) / DEC_WAVES);
+      (int64_t)Hkv * ((int64_t)n_shards * pgroups +
+                      ((int64_t)a.gen_parts * a.row_tiles + DEC_WAVES - 1) / DEC_WAVES);
   if (nwg == 0) return PULSAR_OK;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const size_t lds = (size_t)DEC_WAVES * 2 * DEC_KEYS * d * 2;  // two V stages per wave

@@ -62,6 +62,8 @@ def test_decode_step(G):
     (4, 1, 64, 100, 17, 2, 300),     # the small layer shape, d 64
     (8, 8, 128, 65, 3, 5, 129),      # one query head per KV head
     (16, 8, 64, 31, 0, 6, 77),       # two query heads per KV head
+    (32, 8, 128, 40, 4100, 1, 256),  # generation shard over 4096 rows: attention kernel
+    (64, 1, 64, 3, 10, 1, 100),      # 64 heads per KV head: no 32-row tile, attention kernel
 ])
 def test_shapes(Hq, Hkv, d, Tq, G, ns, S):
     seed = Hq * 7 + Tq + G
