@@ -321,12 +321,15 @@ inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 // one merge folds them all.  With the decode kernel (few query rows) one
 // launch covers the ranges of every shard and of the generation shard (the
 // G appended rows and the new tokens' own).  Otherwise the attention kernel
-// gives the key splits of the shards; a generation shard of at most
-// kGenDecodeRows rows then goes to the decode kernel in 32-row tiles (each
-// token limited to the rows up to its own), and a longer one to the
-// attention kernel: key splits of the G appended rows, and one index-causal
-// partial over the new tokens' own rows.
+// gives the key splits of the shards.  A generation shard of at most
+// kGenDecodeRows rows, for at most kGenDecodeQueryRows (token, head) rows
+// per KV head, then goes to the decode kernel in 32-row tiles (each token
+// limited to the rows up to its own; every tile reads the shard's K/V once,
+// so this is kept to 16 tiles).  Otherwise the attention kernel takes it:
+// key splits of the G appended rows, and one index-causal partial over the
+// new tokens' own rows.
 constexpr int64_t kGenDecodeRows = 4096;
+constexpr int64_t kGenDecodeQueryRows = 512;
 struct QueryPlan {
   bool decode;      // everything in one decode launch
   bool gen_decode;  // the generation shard in a decode launch
@@ -336,7 +339,8 @@ struct QueryPlan {
 QueryPlan query_plan(int n_shards, int Tq, int64_t S, int64_t G, int Hq, int Hkv, int d) {
   QueryPlan p{};
   p.decode = decode_applies(Tq, Hq, Hkv, d);
-  p.gen_decode = p.decode || ((d == 64 || d == 128) && Hq / Hkv <= 32 && G + Tq <= kGenDecodeRows);
+  p.gen_decode = p.decode || ((d == 64 || d == 128) && Hq / Hkv <= 32 && G + Tq <= kGenDecodeRows &&
+                               (int64_t)Tq * (Hq / Hkv) <= kGenDecodeQueryRows);
   if (p.decode) {
     p.np_shard = decode_parts(n_shards, S, Hkv);
   } else {

@@ -64,6 +64,7 @@ def test_decode_step(G):
     (16, 8, 64, 31, 0, 6, 77),       # two query heads per KV head
     (32, 8, 128, 40, 4100, 1, 256),  # generation shard over 4096 rows: attention kernel
     (64, 1, 64, 3, 10, 1, 100),      # 64 heads per KV head: no 32-row tile, attention kernel
+    (32, 8, 128, 130, 20, 1, 64),    # 520 query rows per KV head: attention kernel, G > 0
 ])
 def test_shapes(Hq, Hkv, d, Tq, G, ns, S):
     seed = Hq * 7 + Tq + G
