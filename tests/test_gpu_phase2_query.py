@@ -65,6 +65,8 @@ def test_decode_step(G):
     (32, 8, 128, 40, 4100, 1, 256),  # generation shard over 4096 rows: attention kernel
     (64, 1, 64, 3, 10, 1, 100),      # 64 heads per KV head: no 32-row tile, attention kernel
     (32, 8, 128, 130, 20, 1, 64),    # 520 query rows per KV head: attention kernel, G > 0
+    (64, 8, 64, 13, 7, 2, 90),       # 8 heads per KV head: tiles of 4 tokens, the last of 1
+    (32, 1, 64, 5, 3, 1, 50),        # 32 heads per KV head: one token per tile
 ])
 def test_shapes(Hq, Hkv, d, Tq, G, ns, S):
     seed = Hq * 7 + Tq + G
@@ -92,6 +94,7 @@ def test_peaked_queries():
     (16, 8, 64, 16, 600, 2, 300),    # generation shard in three key ranges
     (32, 8, 128, 3, 2000, 4, 512),   # eight generation ranges, the last holding the new rows
     (4, 1, 64, 7, 0, 1, 100),        # one KV head
+    (32, 1, 128, 1, 40, 2, 333),     # 32 heads per KV head, one token: a full tile
 ])
 def test_few_rows_one_launch(Hq, Hkv, d, Tq, G, ns, S):
     # Tq * Hq / Hkv <= 32: shards and generation shard in one decode launch,
