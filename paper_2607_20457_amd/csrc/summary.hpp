@@ -172,12 +172,18 @@ __device__ __forceinline__ void select_block(const KeyT* cv, int C, uint32_t key
   const int slots = (C + 63) >> 6;
   const int n_slots = S > 0 ? S : slots;
   constexpr int R = S > 0 ? S : 1;
+  // With S > 0 a slot past the block's chunks holds the key 0xFFFFFFFF, so
+  // the tests need no validity term.  A bisection midpoint is always below
+  // key_hi, so such a slot never counts as at or below it, nor below tau.
+  // Should tau itself be 0xFFFFFFFF, these slots are the highest chunk
+  // indices: they rank after every real chunk equal to tau, of which there
+  // are at least k - #(< tau), so none of them is kept.
   uint32_t xr[R];
 #pragma unroll
   for (int i = 0; i < R; ++i)
-    xr[i] = (S > 0 && i < slots && 64 * i + lane < C) ? (uint32_t)cv[64 * i + lane] : 0u;
+    xr[i] = (S > 0 && i < slots && 64 * i + lane < C) ? (uint32_t)cv[64 * i + lane] : 0xFFFFFFFFu;
   // valid: the slot holds a chunk of the block; key: its key
-#define SEL_VALID(i) (64 * (i) + lane < C)
+#define SEL_VALID(i) (S > 0 || 64 * (i) + lane < C)
 #define SEL_KEY(i) (S > 0 ? xr[S > 0 ? (i) : 0] : (uint32_t)cv[64 * (i) + lane])
   uint32_t lo = 0, hi = key_hi;  // #(key <= hi) >= k; tau in [lo, hi]
   while (lo < hi) {
