@@ -9,13 +9,13 @@
 // step has one tile.
 //
 // Work.  Wave w of a workgroup takes key range `part` of one (shard, KV
-// head) for one row tile and writes its own (o, lse) partial; the caller merges the parts of
-// a shard (and then the shards) with the log-sum-exp merge.  In a decode
-// step the generation shard rides in the same launch: workgroups past the
-// shards' take its key ranges, rows [0, G) appended earlier and then the new
-// tokens' own rows, of which token t sees those up to its own (row G + t).
-// A wave streams its keys in 32-key steps, on its own (no workgroup
-// barrier):
+// head) for one row tile; the tiles of a range write disjoint rows of its
+// (o, lse) partial, and the caller merges the partials with the log-sum-exp
+// merge.  The generation shard of a query step (rows [0, G) appended
+// earlier, then the new tokens' own rows) may ride in the same launch:
+// workgroups past the shards' take its key ranges, token t sees rows up to
+// its own (G + t), and a tile's range ends at its last token's row.  A wave
+// streams its keys in 32-key steps, on its own (no workgroup barrier):
 //   K  straight into registers as the A operand of S^T = K Q^T (lane l32
 //      loads key swap_bits23(l32) of the step, so that P comes out in the B
 //      layout of the PV product);
