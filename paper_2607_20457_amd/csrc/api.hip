@@ -313,8 +313,7 @@ int pulsar_lse_merge(const float* o_parts, const float* lse_parts, int H, int Tq
 
 // Phase-2 attention of new tokens: partials of the shards, of the G earlier
 // appended rows and of the new tokens' own rows (causal), then one merge.
-// Workspace: the partials (o, then lse, each 16-byte aligned), then the key
-// split space of the shard pass (the larger of the two unmasked passes).
+// Workspace: the partials, o then lse, each 16-byte aligned.
 namespace {
 inline size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
 // Partials of a Phase-2 query step; every key range is its own partial and
