@@ -95,6 +95,7 @@ def test_peaked_queries():
     (32, 8, 128, 3, 2000, 4, 512),   # eight generation ranges, the last holding the new rows
     (4, 1, 64, 7, 0, 1, 100),        # one KV head
     (32, 1, 128, 1, 40, 2, 333),     # 32 heads per KV head, one token: a full tile
+    (32, 8, 128, 1, 0, 0, 0),        # one token, nothing before it: its own row only
 ])
 def test_few_rows_one_launch(Hq, Hkv, d, Tq, G, ns, S):
     # Tq * Hq / Hkv <= 32: shards and generation shard in one decode launch,
