@@ -8,12 +8,13 @@
 // Rotate-half form: pair i < d/2 of a head vector is (x_i, x_{i+d/2}) and is
 // turned by the angle p * w_i.
 //
-// Thread (row, j) owns pairs 8j .. 8j+7 of every head of its row: 16-byte
-// loads of x[8j .. 8j+7] and x[d/2+8j .. d/2+8j+7], four heads at a time
-// with the next four in flight.  Its eight angles are
-// formed once, in fp64 (p * w_i, then reduced to [-pi, pi] with a two-part
-// 2*pi), and their sine and cosine (fp32, on the reduced angle) serve every
-// head of the row.  The rotation is evaluated in fp32 and rounded once to
+// One wavefront per row.  Lane (h, j) owns pairs 8j .. 8j+7 of heads h,
+// h + 64/(d/16), ...: 16-byte loads of x[8j .. 8j+7] and
+// x[d/2+8j .. d/2+8j+7], so that each load instruction reads contiguous
+// runs of the row.  Each of the row's angles is formed once, in fp64
+// (p * w_i, then reduced to [-pi, pi] with a two-part 2*pi), its sine and
+// cosine taken in fp32 on the reduced angle, and handed to the lanes that
+// use it.  The rotation is evaluated in fp32 and rounded once to
 // bf16.  Bound by HBM: 2 * n_rows * H * d * 2 bytes per call.
 #include <cmath>
 
@@ -41,48 +42,49 @@ __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict
                                                             int64_t rows, int64_t n_rows, int H,
                                                             const int32_t* __restrict__ pos,
                                                             int64_t pos_offset, RopeFreqs f) {
-  constexpr int G = D / 16;  // threads per row
-  constexpr int U = 4;       // heads per batch of loads
-  const int64_t t = (int64_t)blockIdx.x * kRopeThreads + threadIdx.x;
-  const int64_t row = t / G;
-  const int j = (int)(t % G);
-  if (row >= rows) return;
+  constexpr int G = D / 16;     // lanes per head: pairs 8j .. 8j+7 each
+  constexpr int HPW = 64 / G;   // heads per wavefront step
+  constexpr int U = 4;          // steps whose loads are in flight together
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * (kRopeThreads / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;  // wave-uniform
+  const int j = lane % G, hl = lane / G;
   uint16_t* base = X + row * (int64_t)H * D + 8 * j;
-  // Heads go U at a time.  The first batch is loaded before anything else,
-  // so that it travels while the angles are formed, and each later batch is
-  // loaded before the one in hand is rotated and stored.
+  // Heads hl, hl + HPW, ...: one step covers HPW heads of the row, its low
+  // and high halves as two runs of contiguous 16-byte chunks.  Loads are
+  // branch-free (a head past the last re-reads the last; it is not stored).
   u32x4 lo[U], hi[U];
-  // branch-free, so that the compiler can count the loads in flight: a head
-  // past the last one re-reads the last (it is never stored)
   auto load = [&](int h0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int hh = min(h0 + u, H - 1);
+      const int hh = min(h0 + u * HPW + hl, H - 1);
       lo[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D);
       hi[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D + D / 2);
     }
   };
-  // The eight frequencies and the position are requested first and the
-  // first batch of data after them: memory counters retire in order, so
-  // waiting for the frequencies then leaves the data in flight.
-  double w[8];
-#pragma unroll
-  for (int v = 0; v < 8; ++v) w[v] = f.w[8 * j + v];
+  // The row's angles: lane (hl, j) forms that of pair 8j + hl % 8, then
+  // each lane gathers the eight of its own pairs 8j .. 8j+7 from lanes
+  // v * G + j.  The frequency and the position are requested before the
+  // first data, which then stays in flight while the angle is formed.
+  const int pair = 8 * j + (hl & 7);
+  double w = f.w[pair];
   int64_t p = HAS_POS ? (int64_t)pos[row] : row % n_rows;
   load(0);
-#pragma unroll
-  for (int v = 0; v < 8; ++v) asm volatile("" : "+v"(w[v]));
-  asm volatile("" : "+v"(p));
+  asm volatile("" : "+v"(w), "+v"(p));
   p += pos_offset;
-  const double pd = (double)p;
-  float c[8], s[8];
-#pragma unroll
-  for (int v = 0; v < 8; ++v) {
-    const double a = pd * w[v];
+  float s1, c1;
+  {
+    const double a = (double)p * w;
     const double k = rint(a * kInvTwoPi);
     double r = fma(-k, kTwoPiHi, a);
     r = fma(-k, kTwoPiLo, r);
-    sincosf((float)r, &s[v], &c[v]);
+    sincosf((float)r, &s1, &c1);
+  }
+  float c[8], s[8];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    s[v] = __shfl(s1, v * G + j, 64);
+    c[v] = __shfl(c1, v * G + j, 64);
   }
   auto rotate = [&](const u32x4 lo, const u32x4 hi, u32x4& olo, u32x4& ohi) {
 #pragma unroll
@@ -99,22 +101,24 @@ __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict
       ohi[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(yhi, bf16x2));
     }
   };
-  for (int h = 0; h < H; h += U) {
+  for (int h0 = 0; h0 < H; h0 += U * HPW) {
     u32x4 clo[U], chi[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       clo[u] = lo[u];
       chi[u] = hi[u];
     }
-    if (h + U < H) load(h + U);
+    if (h0 + U * HPW < H) load(h0 + U * HPW);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (h + u < H) {
+    for (int u = 0; u < U; ++u) {
+      const int hh = h0 + u * HPW + hl;
+      if (hh < H) {
         u32x4 olo, ohi;
         rotate(clo[u], chi[u], olo, ohi);
-        *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D) = olo;
-        *reinterpret_cast<u32x4*>(base + (int64_t)(h + u) * D + D / 2) = ohi;
+        *reinterpret_cast<u32x4*>(base + (int64_t)hh * D) = olo;
+        *reinterpret_cast<u32x4*>(base + (int64_t)hh * D + D / 2) = ohi;
       }
+    }
   }
 }
 
@@ -139,9 +143,7 @@ int pulsar_rope(void* X, int batch, int64_t n_rows, int H, int d, const int32_t*
     if (!(base > 0.0) || !std::isfinite(base)) return PULSAR_EINVAL;
     for (int i = 0; i < d / 2; ++i) f.w[i] = std::pow(base, -2.0 * i / d);
   }
-  const int G = d / 16;
-  const int64_t threads = rows * G;
-  const int64_t blocks = (threads + kRopeThreads - 1) / kRopeThreads;
+  const int64_t blocks = (rows + kRopeThreads / 64 - 1) / (kRopeThreads / 64);  // a wave per row
   if (blocks > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   auto s = (hipStream_t)stream;
   const auto kern = d == 128 ? (pos ? rope_kernel<128, true> : rope_kernel<128, false>)
