@@ -91,6 +91,8 @@ int pulsar_version(void);
  * chunk_mindf out int32 [batch, num_blocks, Lb / chunk], nullable: the
  *             minimum df of each chunk (IDF of the chunk score = ln(N/mindf)).
  * idf         out float [batch, vocab], nullable: IDF(t) for every id.
+ * A context of no tokens (L == 0, so topk must be 0) has no chunks: nothing
+ * is read and only idf, when given, is written (ln(num_blocks) everywhere).
  *
  * EINVAL: batch < 0, L < 0, num_blocks < 1, L % num_blocks != 0,
  *         Lb % chunk != 0, chunk < 1, topk < 0 or topk > Lb / chunk,

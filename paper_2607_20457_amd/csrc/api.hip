@@ -97,6 +97,11 @@ int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_bl
   if ((int64_t)batch * num_blocks * topk > 0 && sel_chunks == nullptr) return PULSAR_EINVAL;
   if (num_blocks > 255 || !is_pow2(chunk) || chunk < 4 || chunk > 256) return PULSAR_EUNSUPPORTED;
   if (L >= ((int64_t)1 << 31)) return PULSAR_EUNSUPPORTED;
+  if ((int64_t)batch * L == 0) {
+    // no tokens: every df is 0, so IDF(t) = ln(N / 1) and there are no chunks
+    if (batch == 0 || idf == nullptr) return PULSAR_OK;
+    return launch_idf_fill(idf, (int64_t)batch * vocab, num_blocks, (hipStream_t)stream);
+  }
   const size_t lds = maxidf_lds_bytes(L, num_blocks, chunk, vocab);
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
   return launch_maxidf(ids, batch, L, num_blocks, chunk, topk, vocab, sel_chunks, chunk_mindf, idf,

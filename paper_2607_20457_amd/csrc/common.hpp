@@ -181,5 +181,8 @@ int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz
                      int d, int64_t part_ostride, int64_t part_lstride, float* o, float* lse,
                      hipStream_t stream);
 
+// IDF of a context with no tokens: every entry ln(num_blocks / 1).
+int launch_idf_fill(float* idf, int64_t n, int num_blocks, hipStream_t stream);
+
 int launch_copy_rows(const void* src, int64_t src_pitch, void* dst, int64_t dst_pitch,
                      int64_t bytes_per_row, int rows, hipStream_t stream);

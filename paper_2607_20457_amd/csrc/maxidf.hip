@@ -88,7 +88,8 @@ static MaxidfPlan maxidf_plan(int64_t L, int num_blocks, int chunk, int vocab) {
   // L = 8192 * (a power of two up to 16), blocks of a multiple of 8192 ids
   // (so N <= 16 and the rounds per block are a power of two)
   const int64_t res_rounds = L / RES_ROUND_TOKENS;
-  if (vocab <= kFastVocab && L % RES_ROUND_TOKENS == 0 && res_rounds <= RES_ROUNDS &&
+  if (vocab <= kFastVocab && L % RES_ROUND_TOKENS == 0 && res_rounds >= 1 &&
+      res_rounds <= RES_ROUNDS &&
       (res_rounds & (res_rounds - 1)) == 0 && (L / num_blocks) % RES_ROUND_TOKENS == 0 &&
       chunk_bytes <= kResChunkBytes)
     return {kStamp, true, PULSAR_LDS_BYTES, kFastVocab};
@@ -206,10 +207,7 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   // the loads of the next two rounds are in flight while a round's ids are
   // marked, so each thread overlaps its atomics with HBM latency.
   constexpr int ROUND = 2;
-#ifndef MAXIDF_PREFETCH
-#define MAXIDF_PREFETCH 2
-#endif
-  constexpr int PREFETCH = MAXIDF_PREFETCH;  // rounds of loads in flight
+  constexpr int PREFETCH = 2;  // rounds of loads in flight
   const int nvec = Lb >> 2;  // int4 groups per block
   const int4* seq4 = reinterpret_cast<const int4*>(seq);
   const int rpb = (nvec + MAXIDF_THREADS * ROUND - 1) / (MAXIDF_THREADS * ROUND);
@@ -283,10 +281,7 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   // Groups of PF int4 loads per thread, double-buffered: group g+1 is in
   // flight while group g is reduced.  Every lane runs the same trip count,
   // so all lanes join the cross-lane minimum.
-#ifndef MAXIDF_PF2
-#define MAXIDF_PF2 4
-#endif
-  constexpr int PF = MAXIDF_PF2;
+  constexpr int PF = 4;
   const int nvec_seq = (int)(L >> 2);  // L < 2^31 (checked by the caller)
   const int group = chunk >> 2;        // lanes per chunk (1..64)
   const int group_log2 = chunk_log2 - 2;
@@ -532,14 +527,15 @@ static ResidentKernel resident_kernel(int rounds, int chunk_log2) {
     case 8: return resident_for_chunk<8, CARRY_NEXT>(chunk_log2);
     case 4: return resident_for_chunk<4, CARRY_NEXT>(chunk_log2);
     case 2: return resident_for_chunk<2, CARRY_NEXT>(chunk_log2);
-    default: return resident_for_chunk<1, CARRY_NEXT>(chunk_log2);
+    case 1: return resident_for_chunk<1, CARRY_NEXT>(chunk_log2);
+    default: return nullptr;  // maxidf_plan admits only the round counts above
   }
 }
 
 int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
                   int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
                   hipStream_t stream) {
-  if (batch == 0) return PULSAR_OK;
+  if (batch == 0 || L == 0) return PULSAR_OK;
   int chunk_log2 = 0;
   while ((1 << chunk_log2) < chunk) ++chunk_log2;
   const MaxidfPlan plan = maxidf_plan(L, num_blocks, chunk, vocab);
@@ -559,6 +555,7 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
     const int grid = batch < n_cu ? batch : n_cu;
     const ResidentKernel kern = batch > grid ? resident_kernel<true>(rounds, chunk_log2)
                                              : resident_kernel<false>(rounds, chunk_log2);
+    if (kern == nullptr) return PULSAR_EINVAL;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(MAXIDF_THREADS), 0, stream, ids, batch, num_blocks,
                        rpb_log2, chunk_log2, topk, vocab, sel, chunk_mindf, idf);
     return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;

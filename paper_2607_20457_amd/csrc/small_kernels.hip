@@ -58,6 +58,25 @@ int launch_copy_rows(const void* src, int64_t src_pitch, void* dst, int64_t dst_
 }
 
 // ---------------------------------------------------------------------------
+// IDF table of a context without tokens (Eq. idf with df = 0 everywhere):
+// the value the Max-IDF kernels write for an id that occurs in no block.
+__global__ __launch_bounds__(256) void idf_fill_kernel(float* __restrict__ idf, int64_t n,
+                                                       float num_blocks) {
+  const float v = logf(num_blocks / 1.0f);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    idf[i] = v;
+}
+
+int launch_idf_fill(float* idf, int64_t n, int num_blocks, hipStream_t stream) {
+  if (n == 0) return PULSAR_OK;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(idf_fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, idf, n,
+                     (float)num_blocks);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+// ---------------------------------------------------------------------------
 // Online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
 // Thread = four consecutive head_dim entries of one (z, query, head).  One
 // pass over the parts, eight at a time with all their loads issued

@@ -90,6 +90,18 @@ def test_maxidf_validation():
     assert call(batch=0) == 0            # nothing to do
 
 
+@pytest.mark.parametrize("L,N,V", [(0, 4, 16), (0, 16, 32000), (0, 1, 128256)])
+def test_maxidf_empty_context_launches_nothing(L, N, V):
+    # A context of no tokens has no chunks (so k must be 0) and nothing to
+    # read: with NULL ids and outputs the call returns OK on the host without
+    # a launch.  (Before, maxidf_plan picked the register-resident kernel with
+    # zero rounds, which read 8192 ids per sequence from the NULL pointer.)
+    f = _lib.lib().pulsar_maxidf_summaries
+    for batch in (1, 3, 300):
+        assert f(None, batch, L, N, 16, 0, V, None, None, None, None) == 0
+    assert f(None, 1, L, N, 16, 1, V, None, None, None, None) == EINVAL  # k > 0 chunks
+
+
 def test_attention_validation():
     f = _lib.lib().pulsar_phase1_attn
     base = [FAKE, FAKE, FAKE, 1, 4096, 4, 1, 64, 4, 1, 64, 16, 4, FAKE, 0, 0.125,
