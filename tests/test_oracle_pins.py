@@ -284,6 +284,56 @@ def test_phase1_reduces_to_plain_causal():
         np.testing.assert_allclose(o, _sdpa(Q[blk], K[blk], V[blk], True), atol=1e-12)
 
 
+def _sdpa_lse(q, k, scale):
+    """Row log-sum-exp of causal scores, [Hq, n], from torch's logsumexp."""
+    qt = torch.from_numpy(np.asarray(q, dtype=np.float64)).transpose(0, 1)   # [Hq, n, d]
+    kt = torch.from_numpy(np.asarray(k, dtype=np.float64)).transpose(0, 1)   # [Hkv, n, d]
+    kt = kt.repeat_interleave(qt.shape[0] // kt.shape[0], dim=0)
+    s = torch.matmul(qt, kt.transpose(1, 2).contiguous()) * scale
+    n = s.shape[-1]
+    s = s.masked_fill(torch.ones(n, n, dtype=torch.bool).triu(1), float("-inf"))
+    return torch.logsumexp(s, dim=-1).numpy()
+
+
+@pytest.mark.parametrize("i,sink,m,k,Hq,Hkv", [(3, 16, 16, 3, 4, 1), (2, 20, 10, 2, 8, 2),
+                                                (1, 8, 8, 4, 4, 4)])
+def test_phase1_sampled_rows_match_full_pass_and_sdpa(i, sink, m, k, Hq, Hkv):
+    # The sampled-row form of Phase-1 attention (used for the long inputs)
+    # against (a) the full pass restricted to those rows and (b) PyTorch's
+    # fp64 SDPA over the assembled input [S_sink || Sigma_0..Sigma_{i-1} ||
+    # B_i] (Eq. 3, Eq. 1).  Sigma_0 holds chunk 0 of B_0, which duplicates
+    # the sink, so rows with equal positions occur; rows are unsorted and
+    # include the first, the last, sink, summary and block rows.
+    rng = np.random.default_rng(100 + i)
+    L, N, d = 4 * 160, 4, 16
+    Lb = L // N
+    Q = rng.standard_normal((L, Hq, d))
+    K = rng.standard_normal((L, Hkv, d))
+    V = rng.standard_normal((L, Hkv, d))
+    sel = np.array([np.sort(rng.choice(Lb // m, k, replace=False)) for _ in range(N)])
+    # Sigma_0 starts with chunk 0, the sink's own tokens
+    sel[0] = np.concatenate([[0], np.sort(rng.choice(np.arange(1, Lb // m), k - 1,
+                                                     replace=False))])
+    pos = assembly.phase1_positions(L, N, i, sink, m, k, sel)
+    n = len(pos)
+    assert n == Lb + sink + i * k * m
+    assert len(set(pos[:sink]) & set(pos[sink:sink + m])) > 0   # a duplicate exists
+    scale = 1 / math.sqrt(d)
+    rows = np.array([n - 1, 0, sink - 1, sink, sink + m - 1, n - Lb - 1, n - Lb, n // 2, 5])
+    o_s, lse_s = attention.phase1_attention(Q, K, V, pos, scale, rows=rows)
+    o_f, lse_f = attention.phase1_attention(Q, K, V, pos, scale)
+    np.testing.assert_allclose(o_s, o_f[rows], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse_s, lse_f[:, rows], atol=1e-12, rtol=0)
+    # independent of the oracle's attention code: assemble by indexing, SDPA
+    qa, ka, va = Q[pos], K[pos], V[pos]
+    np.testing.assert_allclose(o_s, _sdpa(qa, ka, va, True)[rows], atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse_s, _sdpa_lse(qa, ka, scale)[:, rows], atol=1e-12, rtol=0)
+    # the same row with its own key dropped (an off-by-one in the key range)
+    # is far from it, so the comparisons above can see such a mistake
+    o_bad, _ = attention.causal_attention_rows(qa, ka[:n - 1], va[:n - 1], scale, [n - 1])
+    assert np.max(np.abs(o_bad[0] - o_s[0])) > 1e-6
+
+
 def test_partial_matches_sdpa_and_empty_shard():
     rng = np.random.default_rng(3)
     q = rng.standard_normal((5, 8, 32))
