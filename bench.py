@@ -12,14 +12,17 @@ Llama-3.1-8B-shaped layer (32 query / 8 KV heads, head_dim 128, bf16):
      shards of 8192 keys, and the online-softmax merge.
 
 Inputs are synthetic (Zipf(1.1) ids over 128256, bf16 N(0,1) Q/K/V) and
-already resident in HBM when timing starts.  The JSON line reports the whole
-step's attention FLOP rate as ``value``, per-kernel rates measured with HIP
-events on the launch stream, the roofline of the dominant kernel (Phase-1
-attention, bf16 MFMA bound), the Star Attention anchor baseline measured the
-same way, and the fp64 CPU oracle timed on a bounded sample.
+already resident in HBM when timing starts.  The JSON line reports the Phase-1
+attention FLOP rate of block 15 as ``value`` (the metric), per-kernel rates
+measured with HIP events on the launch stream, the roofline of that dominant
+kernel (bf16 MFMA bound), the Star Attention anchor baseline for the same
+block, the anchor-vs-Pulsar sweep (batch 4 x 128K, all 16 blocks, top-k
+8/32/64) beside the cost model's ratios, Max-IDF at batch 8 and 1024, and the
+fp64 CPU oracle timed on a bounded sample.
 
-``--sweep`` instead prints one JSON line with the anchor-vs-Pulsar sweep
-(batch 4, all 16 blocks, top-k 8/32/64) and the Max-IDF batch sweep.
+``--profile-step`` runs only the warm-up and timed steps (for profiler
+traces whose rows then hold the step's launches alone).  ``--sweep`` prints
+the anchor-vs-Pulsar sweep and a wider Max-IDF batch sweep instead.
 """
 from __future__ import annotations
 
@@ -139,6 +142,7 @@ def cpu_oracle_baseline(ids, q, k, v, sel_ref, cfg, n, budget_s=15.0):
 
 
 IDF_THROUGHPUT_BATCH = 1024
+METRIC = "Phase-1 prefixed-block attn TFLOP/s (% bf16 MFMA peak); Max-IDF tokens/s"
 
 
 def run_main(args):
@@ -184,6 +188,18 @@ def run_main(args):
     end.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / args.steps
+
+    f_p1 = causal_flops(n, cfg.Hq, cfg.d)
+    f_p2 = full_flops(Tq, N * cfg.Lb, cfg.Hq, cfg.d)
+    p1_ms = t_p1.mean_ms()
+    p1_tflops = f_p1 / (p1_ms * 1e-3) / 1e12
+    if args.profile_step:
+        print(json.dumps({"metric": METRIC, "value": p1_tflops, "unit": "TFLOP/s",
+                          "ms_per_step": ms_step, "phase1_attn_ms": p1_ms,
+                          "phase2_partial_merge_ms": t_p2.mean_ms(),
+                          "maxidf_ms": t_idf.mean_ms(), "steps": args.steps,
+                          "warmup": args.warmup}), flush=True)
+        return
 
     # Star Attention anchor baseline for the same block, timed the same way
     for _ in range(2):
@@ -270,17 +286,29 @@ def run_main(args):
     torch.cuda.synchronize()
     kv_bytes = 2 * N * cfg.Lb * cfg.Hkv * cfg.d * 2
 
-    f_p1 = causal_flops(n, cfg.Hq, cfg.d)
+    # Max-IDF at batch 8 (the sweep's setting): latency-bound, 8 compute units
+    t_idf8 = Timer()
+    ids8 = workload.make_ids(workload.CONFIGS["sweep_128k_b4"], batch=8)
+    d_ids8 = torch.from_numpy(ids8).cuda()
+    P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab)
+    for _ in range(5):
+        with t_idf8:
+            P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab)
+    torch.cuda.synchronize()
+
     f_star = causal_flops(n_star, cfg.Hq, cfg.d)
-    f_p2 = full_flops(Tq, N * cfg.Lb, cfg.Hq, cfg.d)
-    p1_ms, p2_ms, idf_ms, star_ms = t_p1.mean_ms(), t_p2.mean_ms(), t_idf.mean_ms(), t_star.mean_ms()
-    p1_tflops = f_p1 / (p1_ms * 1e-3) / 1e12
+    p2_ms, idf_ms, star_ms = t_p2.mean_ms(), t_idf.mean_ms(), t_star.mean_ms()
     idf_bytes = cfg.L * 4 + N * cfg.topk * 4
     p2_bytes = 2 * N * cfg.Lb * cfg.Hkv * cfg.d * 2 + Tq * cfg.Hq * cfg.d * 2 \
         + 2 * N * Tq * cfg.Hq * (cfg.d + 1) * 4
+    sweep = None
+    if not args.no_sweep:
+        del O, O_star
+        torch.cuda.empty_cache()
+        sweep, _ = cfg5_sweep(reps=2)
     result = {
-        "metric": "Phase-1 prefixed-block attn TFLOP/s (% bf16 MFMA peak); Max-IDF tokens/s",
-        "value": (f_p1 + f_p2) / (ms_step * 1e-3) / 1e12,
+        "metric": METRIC,
+        "value": p1_tflops,
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -298,12 +326,18 @@ def run_main(args):
                    "Hq": cfg.Hq, "Hkv": cfg.Hkv, "head_dim": cfg.d, "seq_len": cfg.L,
                    "batch": 1, "parallelism": "single GPU"},
         "kernels": {
+            "step_attn_tflops": (f_p1 + f_p2) / (ms_step * 1e-3) / 1e12,
             "phase1_attn_ms": p1_ms,
             "phase1_attn_tflops": p1_tflops,
             "phase1_pct_bf16_peak": 100 * p1_tflops / PEAK_BF16_TFLOPS,
             "maxidf_ms": idf_ms,
             "maxidf_tokens_per_s": cfg.L / (idf_ms * 1e-3),
             "maxidf_gbps_algorithmic": idf_bytes / (idf_ms * 1e-3) / 1e9,
+            "maxidf_batch8": {
+                "ms": t_idf8.mean_ms(),
+                "tokens_per_s": 8 * cfg.L / (t_idf8.mean_ms() * 1e-3),
+                "gbps_algorithmic": 8 * idf_bytes / (t_idf8.mean_ms() * 1e-3) / 1e9,
+            },
             "maxidf_throughput": {
                 "batch": IDF_THROUGHPUT_BATCH,
                 "ms": t_idf_big.mean_ms(),
@@ -335,6 +369,7 @@ def run_main(args):
             "flop_ratio_star_over_pulsar": f_star / f_p1,
             "time_ratio_star_over_pulsar": star_ms / p1_ms,
         },
+        "sweep_cfg5": sweep,
         "roofline": {
             "bound": "mfma",
             "achieved": p1_tflops,
@@ -363,7 +398,20 @@ def run_main(args):
     print(json.dumps(result), flush=True)
 
 
-def run_sweep(args):
+# Star/Pulsar Phase-1 FLOP ratios of the cost model (F(n) proportional to n^2,
+# Table 4's accounting) at 16 blocks of 8192, sink 64, chunk 32: the last
+# block and the sum over all 16 blocks, per top-k
+def model_ratios(topk, L=131072, N=16, sink=64, chunk=32):
+    Lb = L // N
+    star = [Lb] + [2 * Lb] * (N - 1)
+    pul = [Lb] + [Lb + sink + i * topk * chunk for i in range(1, N)]
+    return (star[-1] ** 2 / pul[-1] ** 2,
+            sum(x * x for x in star) / sum(x * x for x in pul))
+
+
+def cfg5_sweep(reps=3):
+    """Anchor vs Pulsar Phase-1 over all 16 blocks, batch 4 x 131072 tokens,
+    top-k 8/32/64 (bf16 O, no LSE), each launch timed with HIP events."""
     cfg = workload.CONFIGS["sweep_128k_b4"]
     N, B = cfg.num_blocks, cfg.batch
     ids = workload.make_ids(cfg, batch=B)
@@ -371,8 +419,8 @@ def run_sweep(args):
     Q, K, V = bf16_dev(q), bf16_dev(k), bf16_dev(v)
     del q, k, v
     d_ids = torch.from_numpy(ids).cuda()
-    out = {"metric": "anchor vs Pulsar Phase-1 sweep; Max-IDF batch sweep", "config": {
-        "workload": "batch 4 x 131072 tokens, 16 blocks x 8192, Llama-3.1-8B layer shape"}}
+    out = {"workload": "batch 4 x 131072 tokens, 16 blocks x 8192, sink 64, chunk 32, "
+                       "Llama-3.1-8B layer shape; every block's Phase-1, bf16 O"}
     rows = []
     star_flops, star_ms = 0, 0.0
     for i in range(N):
@@ -381,12 +429,13 @@ def run_sweep(args):
         P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, 0, None, P.PREFIX_ANCHOR,
                       o_dtype=P.OUT_BF16, return_lse=False, out=O)
         t = Timer()
-        for _ in range(3):
+        for _ in range(reps):
             with t:
                 P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, 0, None, P.PREFIX_ANCHOR,
                               o_dtype=P.OUT_BF16, return_lse=False, out=O)
         torch.cuda.synchronize()
         star_ms += t.mean_ms()
+        star_last_ms = t.mean_ms()
         star_flops += B * causal_flops(n_s, cfg.Hq, cfg.d)
         del O
     for topk in (8, 32, 64):
@@ -398,7 +447,7 @@ def run_sweep(args):
             P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, topk, sel, o_dtype=P.OUT_BF16,
                           return_lse=False, out=O)
             t = Timer()
-            for _ in range(3):
+            for _ in range(reps):
                 with t:
                     P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, topk, sel,
                                   o_dtype=P.OUT_BF16, return_lse=False, out=O)
@@ -408,15 +457,31 @@ def run_sweep(args):
             last = (n_i, t.mean_ms(), B * causal_flops(n_i, cfg.Hq, cfg.d))
             del O
         n_s = 2 * cfg.Lb
+        model_last, model_all = model_ratios(topk, cfg.L, N, cfg.sink, cfg.chunk)
         rows.append({"topk": topk, "sigma": topk * cfg.chunk, "pulsar_ms_all_blocks": ms,
                      "pulsar_tflops": fl / (ms * 1e-3) / 1e12,
                      "flop_ratio_star_over_pulsar_all_blocks": star_flops / fl,
                      "time_ratio_star_over_pulsar_all_blocks": star_ms / ms,
+                     "model_ratio_all_blocks": model_all,
                      "last_block_rows": last[0],
+                     "last_block_ms": last[1],
                      "flop_ratio_star_over_pulsar_last_block":
-                         causal_flops(n_s, cfg.Hq, cfg.d) / causal_flops(last[0], cfg.Hq, cfg.d)})
-    out["anchor"] = {"ms_all_blocks": star_ms, "tflops": star_flops / (star_ms * 1e-3) / 1e12}
+                         causal_flops(n_s, cfg.Hq, cfg.d) / causal_flops(last[0], cfg.Hq, cfg.d),
+                     "time_ratio_star_over_pulsar_last_block": star_last_ms / last[1],
+                     "model_ratio_last_block": model_last})
+    out["anchor"] = {"ms_all_blocks": star_ms, "last_block_ms": star_last_ms,
+                     "tflops": star_flops / (star_ms * 1e-3) / 1e12}
     out["pulsar"] = rows
+    del Q, K, V
+    torch.cuda.empty_cache()
+    return out, ids
+
+
+def run_sweep(args):
+    out, ids = cfg5_sweep()
+    out = {"metric": "anchor vs Pulsar Phase-1 sweep; Max-IDF batch sweep", "config": out}
+    cfg = workload.CONFIGS["sweep_128k_b4"]
+    N, B = cfg.num_blocks, cfg.batch
     # Max-IDF over batches of 128K sequences: latency-bound at small batch,
     # HBM-bound once the ids no longer fit the caches
     idf_rows = []
@@ -455,6 +520,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="leave the anchor-vs-Pulsar sweep out of the default run")
+    ap.add_argument("--profile-step", action="store_true",
+                    help="only the warm-up and timed steps (for profiler traces)")
     ap.add_argument("--calibrate", action="store_true",
                     help="append a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     args = ap.parse_args()

@@ -16,10 +16,15 @@ items are not used):
   uniformly drawn positions, so that each needle has document frequency 1.
 * Q/K/V: float32 N(0,1) from PCG64, rounded to bfloat16 with round-to-nearest-
   even, returned as the raw uint16 bit patterns in ``[batch, L, heads, d]``.
+  The flat array is drawn in pieces of 2^24 values; piece j comes from its own
+  PCG64 stream seeded with (seed, j), so the pieces can be drawn by several
+  threads and the result does not depend on how many.
 """
 from __future__ import annotations
 
+import concurrent.futures as _cf
 import dataclasses
+import os
 
 import numpy as np
 
@@ -79,13 +84,31 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
+PIECE = 1 << 24  # values per independently seeded piece of a bf16_normal draw
+
+
 def bf16_normal(seed: int, shape, scale: float = 1.0) -> np.ndarray:
     """bf16 bit patterns of ``scale * N(0,1)`` float32 samples."""
-    rng = _rng(seed)
-    x = rng.standard_normal(size=shape, dtype=np.float32)
-    if scale != 1.0:
-        x *= np.float32(scale)
-    return f32_to_bf16_bits(x)
+    out = np.empty(int(np.prod(shape, dtype=np.int64)), dtype=np.uint16)
+
+    def piece(j: int) -> None:
+        lo = j * PIECE
+        hi = min(out.size, lo + PIECE)
+        rng = np.random.Generator(np.random.PCG64([seed, j]))
+        x = rng.standard_normal(size=hi - lo, dtype=np.float32)
+        if scale != 1.0:
+            x *= np.float32(scale)
+        out[lo:hi] = f32_to_bf16_bits(x)
+
+    n_pieces = (out.size + PIECE - 1) // PIECE
+    workers = max(1, min(n_pieces, len(os.sched_getaffinity(0)), 16))
+    if workers == 1:
+        for j in range(n_pieces):
+            piece(j)
+    else:
+        with _cf.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(piece, range(n_pieces)))
+    return out.reshape(shape)
 
 
 @dataclasses.dataclass(frozen=True)

@@ -43,3 +43,16 @@ def check_attention(o_gpu, lse_gpu, o_ref, lse_ref, what=""):
         assert np.array_equal(np.isfinite(lse_gpu), finite), f"{what}: LSE infinities differ"
         lerr = np.max(np.abs(lse_gpu[finite] - lse_ref[finite])) if finite.any() else 0.0
         assert lerr <= LSE_ATOL, f"{what}: LSE max-abs error {lerr}"
+
+
+def check_attention_bf16(o_gpu_bf16, o_ref, what=""):
+    """A bf16 output is the fp32 result rounded once: the O bounds widen by
+    half a bf16 ulp of the reference value (2^-9 relative)."""
+    o = np.asarray(o_gpu_bf16, dtype=np.float64)
+    err = np.abs(o - o_ref)
+    bound = O_ATOL + np.abs(o_ref) * 2.0 ** -9
+    assert np.all(err <= bound), f"{what}: O error {np.max(err - bound) + O_ATOL} above bound"
+    nrm = np.linalg.norm(o_ref)
+    if nrm > 0:
+        rel = np.linalg.norm(o - o_ref) / nrm
+        assert rel <= O_REL_L2 + 2.0 ** -9, f"{what}: O relative L2 error {rel}"

@@ -10,7 +10,8 @@ import torch
 import paper_2607_20457_amd as P
 from oracle import assembly, attention, maxidf
 from paper_2607_20457_amd import workload
-from tests._helpers import check_attention, f64, gpu_available, to_dev_bf16, to_dev_i32
+from tests._helpers import (check_attention, check_attention_bf16, f64, gpu_available,
+                            to_dev_bf16, to_dev_i32)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -188,3 +189,130 @@ def test_even_spaced_positions_match_the_oracle(Lb, sink, m, k):
                                  device="cuda").cpu().numpy()
         ref = assembly.phase1_positions(N * Lb, N, i, sink, m, k, None, assembly.PREFIX_EVEN)
         assert np.array_equal(pos[0], ref) and np.array_equal(pos[1], ref)
+
+
+def _oracle_rows(cfg, i, mode, sel_b, q_b, k_b, v_b, rows, topk=None):
+    topk = cfg.topk if topk is None else topk
+    pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, topk,
+                                    sel_b, mode)
+    rows = np.array(sorted(set(int(r) for r in rows if 0 <= r < len(pos))))
+    # fp64 copies of only the positions the sampled rows read (np.zeros
+    # commits no memory for the rest)
+    qp, kp = pos[rows], pos[:rows.max() + 1]
+    Qf, Kf, Vf = np.zeros(q_b.shape), np.zeros(k_b.shape), np.zeros(v_b.shape)
+    Qf[qp], Kf[kp], Vf[kp] = f64(q_b[qp]), f64(k_b[kp]), f64(v_b[kp])
+    o_ref, _ = attention.phase1_attention(Qf, Kf, Vf, pos, 1 / math.sqrt(cfg.d), rows=rows)
+    return rows, o_ref
+
+
+def test_llama8b_128k_block15_bench_launch_no_lse():
+    # Exactly the launch the benchmark times: block 15 of 16, fp32 O into a
+    # caller buffer, no LSE (the kernel build without the fp32 weight sum),
+    # with the retained KV(B_15) copied out; then the Even-Spaced and Star
+    # launches the benchmark times the same way.
+    cfg = workload.CONFIGS["llama8b_128k"]
+    sel, q, k, v = _inputs(cfg)
+    N, i = cfg.num_blocks, cfg.num_blocks - 1
+    n = P.phase1_len(cfg.L, N, i, cfg.sink, cfg.chunk, cfg.topk)
+    Q, K, V, S = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), to_dev_i32(sel)
+    O = torch.empty((1, n, cfg.Hq, cfg.d), dtype=torch.float32, device="cuda")
+    print(f"phase1 bench launch: {cfg.name} block {i} n={n} no LSE, keep KV", flush=True)
+    res = P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, cfg.topk, S, out=O,
+                        return_lse=False, keep_kv=True)
+    torch.cuda.synchronize()
+    assert res[0] is O and len(res) == 3
+    Kk, Vk = res[1], res[2]
+    rng = np.random.default_rng(151)
+    rows = [0, 63, 64, 65, 1087, 1088, 15423, 15424, n - 8193, n - 8192, n - 2, n - 1] + \
+        list(rng.integers(0, n, 40))
+    rows, o_ref = _oracle_rows(cfg, i, P.PREFIX_SUMMARY, sel[0], q[0], k[0], v[0], rows)
+    check_attention(O[0, rows].cpu().numpy(), None, o_ref, None, "128K block 15, no LSE")
+    # KV(B_15): the last Lb rows of Input_15 are block 15's own tokens, bit for bit
+    Lb = cfg.Lb
+    assert torch.equal(Kk.cpu().view(torch.int16),
+                       torch.from_numpy(k[:, i * Lb:(i + 1) * Lb].view(np.int16)))
+    assert torch.equal(Vk.cpu().view(torch.int16),
+                       torch.from_numpy(v[:, i * Lb:(i + 1) * Lb].view(np.int16)))
+    # no-LSE and LSE builds give the same O
+    o_lse, _ = P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, cfg.topk, S)
+    torch.cuda.synchronize()
+    d = (o_lse[0, rows] - O[0, rows]).abs().max().item()
+    assert d <= 1e-3, d
+    del o_lse
+    for mode in (P.PREFIX_EVEN, P.PREFIX_ANCHOR):
+        n_m = P.phase1_len(cfg.L, N, i, cfg.sink, cfg.chunk, cfg.topk, mode)
+        Om = torch.empty((1, n_m, cfg.Hq, cfg.d), dtype=torch.float32, device="cuda")
+        print(f"phase1 bench launch: mode {mode} n={n_m} no LSE", flush=True)
+        P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, cfg.topk, None, mode, out=Om,
+                      return_lse=False)
+        torch.cuda.synchronize()
+        rows_m = [0, 63, 64, 8191, 8192, n_m - 8193, n_m - 1] + list(rng.integers(0, n_m, 20))
+        rows_m, o_ref = _oracle_rows(cfg, i, mode, None, q[0], k[0], v[0], rows_m)
+        check_attention(Om[0, rows_m].cpu().numpy(), None, o_ref, None,
+                        f"128K block 15 mode {mode}, no LSE")
+
+
+_SWEEP = {}
+
+
+def _sweep_inputs():
+    # batch 4 x 131072 tokens of the 8B layer (the anchor-vs-Pulsar sweep)
+    if not _SWEEP:
+        cfg = workload.CONFIGS["sweep_128k_b4"]
+        ids = workload.make_ids(cfg)
+        q, k, v = workload.make_qkv(cfg)
+        _SWEEP.update(cfg=cfg, ids=ids, q=q, k=k, v=v, Q=to_dev_bf16(q), K=to_dev_bf16(k),
+                      V=to_dev_bf16(v))
+    return _SWEEP
+
+
+@pytest.mark.parametrize("topk", [8, 64])
+def test_sweep_batch4_bf16_no_lse(topk):
+    # The sweep's launches: batch 4, bf16 O, no LSE, top-k 8 and 64 (at 64,
+    # block 15 has n = 38976 rows and a 960-run table); rows sampled from two
+    # sequences of the batch, selection checked bit for bit first.
+    w = _sweep_inputs()
+    cfg = w["cfg"]
+    N = cfg.num_blocks
+    sel = P.maxidf_summaries(torch.from_numpy(w["ids"]).cuda(), N, cfg.chunk, topk, cfg.vocab)
+    torch.cuda.synchronize()
+    sel_ref, _, _, _ = maxidf.maxidf_summaries(w["ids"], N, cfg.chunk, topk, cfg.vocab)
+    assert np.array_equal(sel.cpu().numpy(), sel_ref)
+    rng = np.random.default_rng(topk)
+    for i in (1, 8, N - 1):
+        n = P.phase1_len(cfg.L, N, i, cfg.sink, cfg.chunk, topk)
+        O = torch.empty((cfg.batch, n, cfg.Hq, cfg.d), dtype=torch.bfloat16, device="cuda")
+        print(f"sweep launch: batch {cfg.batch} block {i} top-k {topk} n={n} bf16 no LSE",
+              flush=True)
+        P.phase1_attn(w["Q"], w["K"], w["V"], N, i, cfg.sink, cfg.chunk, topk, sel,
+                      o_dtype=P.OUT_BF16, return_lse=False, out=O)
+        torch.cuda.synchronize()
+        for b in (1, 3):
+            rows = [0, 63, 64, n - cfg.Lb - 1, n - cfg.Lb, n - 1] + list(rng.integers(0, n, 10))
+            rows, o_ref = _oracle_rows(cfg, i, P.PREFIX_SUMMARY, sel_ref[b], w["q"][b], w["k"][b],
+                                       w["v"][b], rows, topk=topk)
+            check_attention_bf16(O[b, rows].float().cpu().numpy(), o_ref,
+                                 f"sweep b={b} block {i} k={topk}")
+        del O
+
+
+def test_sweep_batch4_anchor_bf16_no_lse():
+    w = _sweep_inputs()
+    cfg = w["cfg"]
+    N = cfg.num_blocks
+    rng = np.random.default_rng(5)
+    for i in (1, N - 1):
+        n = P.phase1_len(cfg.L, N, i, cfg.sink, cfg.chunk, 0, P.PREFIX_ANCHOR)
+        O = torch.empty((cfg.batch, n, cfg.Hq, cfg.d), dtype=torch.bfloat16, device="cuda")
+        print(f"sweep anchor launch: batch {cfg.batch} block {i} n={n} bf16 no LSE", flush=True)
+        P.phase1_attn(w["Q"], w["K"], w["V"], N, i, cfg.sink, cfg.chunk, 0, None,
+                      P.PREFIX_ANCHOR, o_dtype=P.OUT_BF16, return_lse=False, out=O)
+        torch.cuda.synchronize()
+        for b in (0, 2):
+            rows = [0, 8191, 8192, n - 1] + list(rng.integers(0, n, 8))
+            rows, o_ref = _oracle_rows(cfg, i, P.PREFIX_ANCHOR, None, w["q"][b], w["k"][b],
+                                       w["v"][b], rows, topk=0)
+            check_attention_bf16(O[b, rows].float().cpu().numpy(), o_ref,
+                                 f"sweep anchor b={b} block {i}")
+        del O
+    _SWEEP.clear()
