@@ -18,7 +18,8 @@
  *   [batch, tokens, heads, head_dim].  Element offsets are computed in 64 bits.
  * - bf16 tensors are passed as raw 16-bit storage (IEEE bfloat16).
  * - Return codes are pulsar_status values; 0 is success.
- * - The library keeps no mutable global state; calls on different streams
+ * - The library keeps no mutable global state, apart from the static scratch
+ *   of pulsar_phase2_query_noalloc (see there); calls on different streams
  *   may run concurrently as long as their output buffers do not overlap.
  */
 #ifndef PULSAR_H_
@@ -36,7 +37,8 @@ typedef enum {
   PULSAR_EINVAL = -1,        /* an argument is out of range or a required pointer is NULL */
   PULSAR_EUNSUPPORTED = -2,  /* valid by the paper's definition but outside what this build runs */
   PULSAR_EHIP = -3,          /* the HIP runtime reported an error at launch */
-  PULSAR_EWORKSPACE = -4     /* the workspace is NULL or smaller than the size query returned */
+  PULSAR_EWORKSPACE = -4,    /* the workspace is NULL or smaller than the size query returned */
+  PULSAR_ETOOLARGE = -5      /* the no-allocation call's partials exceed its static scratch */
 } pulsar_status;
 
 typedef enum {
@@ -291,6 +293,32 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
                         const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
                         float softmax_scale, float* o, float* lse, void* workspace,
                         size_t workspace_bytes, void* stream);
+
+/*
+ * Phase-2 attention of new tokens without any allocation, for callers that
+ * cannot allocate device memory or pass a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.
+ *
+ * Arguments, results and errors are those of pulsar_phase2_query without the
+ * workspace.  The partials live in a static device array of
+ * PULSAR_STATIC_SCRATCH_BYTES bytes, one per GPU, held from the library's
+ * first use on that GPU until the process ends; its address is looked up
+ * once per device on the first call made with that device current.  The
+ * call allocates nothing (no hipMalloc, no library allocation).
+ *
+ * ETOOLARGE: pulsar_phase2_query_workspace_bytes(...) for these shapes
+ *   exceeds PULSAR_STATIC_SCRATCH_BYTES (about 33 partials of 64 tokens x 32
+ *   heads x 128 fit, e.g. a 64-token query encoding over 16 shards).
+ * Every call on one GPU uses that GPU's one array: calls that overlap in time
+ * on the same GPU (different streams, or host threads without ordering) race
+ * and give undefined results.  Calls ordered on one stream are safe; nothing
+ * in the array needs to start at zero.
+ */
+#define PULSAR_STATIC_SCRATCH_BYTES (64u << 20)
+int pulsar_phase2_query_noalloc(const void* q, const void* Kg, const void* Vg, int64_t G,
+                                const void* K, const void* V, int n_shards, int Tq, int64_t S,
+                                int Hq, int Hkv, int d, float softmax_scale, float* o, float* lse,
+                                void* stream);
 
 /*
  * Rotary position embedding of query or key rows at given positions

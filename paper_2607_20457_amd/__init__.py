@@ -8,4 +8,4 @@ from .api import (OUT_BF16, OUT_F32, PREFIX_ANCHOR, PREFIX_EVEN, PREFIX_SUMMARY,
                   SCORE_BM25,
                   SCORE_ENTROPY, SCORE_MAXIDF, SCORE_TFIDF, chunk_summaries, lse_merge,
                   maxidf_summaries, phase1_attn, phase1_len, phase1_positions, phase2_partial,
-                  phase2_query, phase2_workspace_bytes, rope_)
+                  phase2_query, phase2_query_noalloc, phase2_workspace_bytes, rope_)

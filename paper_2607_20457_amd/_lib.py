@@ -36,6 +36,9 @@ SIGNATURES = {
     "pulsar_phase2_query": (_c_int, [_vp, _vp, _vp, _c_i64, _vp, _vp, _c_int, _c_int, _c_i64,
                                      _c_int, _c_int, _c_int, _c_float, _vp, _vp, _vp, _c_size,
                                      _vp]),
+    "pulsar_phase2_query_noalloc": (_c_int, [_vp, _vp, _vp, _c_i64, _vp, _vp, _c_int, _c_int,
+                                             _c_i64, _c_int, _c_int, _c_int, _c_float, _vp, _vp,
+                                             _vp]),
     "pulsar_rope": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _vp, _c_i64, _vp,
                              ctypes.c_double, _vp]),
 }

@@ -250,3 +250,31 @@ def phase2_query(q, Kg, Vg, G: int, K=None, V=None, softmax_scale: float | None 
                                         _ptr(workspace), need, _stream())
     _lib.check(st, "pulsar_phase2_query")
     return o, lse
+
+
+def phase2_query_noalloc(q, Kg, Vg, G: int, K=None, V=None, softmax_scale: float | None = None):
+    """``phase2_query`` through the entry point that allocates nothing: the
+    partials live in the library's static per-device scratch.  The outputs
+    are allocated here by torch, as for every binding."""
+    _need(q, torch.bfloat16, "q")
+    _need(Kg, torch.bfloat16, "Kg")
+    _need(Vg, torch.bfloat16, "Vg")
+    Tq, Hq, d = q.shape
+    Hkv = Kg.shape[1]
+    if Kg.shape != (G + Tq, Hkv, d) or Vg.shape != Kg.shape:
+        raise ValueError("Kg/Vg must be [G + Tq, Hkv, d]")
+    n_shards, S = 0, 0
+    if K is not None:
+        _need(K, torch.bfloat16, "K")
+        _need(V, torch.bfloat16, "V")
+        n_shards, S = K.shape[0], K.shape[1]
+        if K.shape != (n_shards, S, Hkv, d) or V.shape != K.shape:
+            raise ValueError("K/V must be [n_shards, S, Hkv, d]")
+    scale = 1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale
+    o = torch.empty((Tq, Hq, d), dtype=torch.float32, device=q.device)
+    lse = torch.empty((Hq, Tq), dtype=torch.float32, device=q.device)
+    st = _lib.lib().pulsar_phase2_query_noalloc(_ptr(q), _ptr(Kg), _ptr(Vg), G, _ptr(K), _ptr(V),
+                                                n_shards, Tq, S, Hq, Hkv, d, scale, _ptr(o),
+                                                _ptr(lse), _stream())
+    _lib.check(st, "pulsar_phase2_query_noalloc")
+    return o, lse

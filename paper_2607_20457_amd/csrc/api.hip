@@ -2,12 +2,13 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.hpp"
 
 namespace {
 
-constexpr int kVersion = 2;
+constexpr int kVersion = 3;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -79,6 +80,7 @@ const char* pulsar_status_string(int status) {
     case PULSAR_EUNSUPPORTED: return "unsupported configuration";
     case PULSAR_EHIP: return "HIP runtime error";
     case PULSAR_EWORKSPACE: return "workspace missing or too small";
+    case PULSAR_ETOOLARGE: return "partials exceed the static scratch of the no-allocation call";
     default: return "unknown status";
   }
 }
@@ -402,10 +404,13 @@ size_t pulsar_phase2_query_workspace_bytes(int n_shards, int Tq, int64_t S, int6
   return align16(parts * Tq * Hq * d * 4) + align16(parts * Hq * Tq * 4);
 }
 
-int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
-                        const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
-                        float softmax_scale, float* o, float* lse, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+// Host-side checks of a Phase-2 query step, everything but the workspace.
+int phase2_query_check(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
+                       const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
+                       float softmax_scale, const float* o) {
   if (n_shards < 0 || Tq < 0 || S < 0 || G < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || d < 1)
     return PULSAR_EINVAL;
   if (!(softmax_scale > 0.f) || !isfinite(softmax_scale)) return PULSAR_EINVAL;
@@ -419,6 +424,43 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   if (q == nullptr || Kg == nullptr || Vg == nullptr || o == nullptr) return PULSAR_EINVAL;
   if (n_shards > 0 && S > 0 && (K == nullptr || V == nullptr)) return PULSAR_EINVAL;
   if (!aligned16(q) || !aligned16(Kg) || !aligned16(Vg) || !aligned16(o)) return PULSAR_EINVAL;
+  return PULSAR_OK;
+}
+
+// The no-allocation variant's partials: one array per device, for the life
+// of the process.  In host code `scratch` names a host-side stand-in; the
+// device address comes from hipGetSymbolAddress, once per device, and only
+// that address is ever handed to a kernel.
+__device__ __align__(256) uint8_t scratch[PULSAR_STATIC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices];  // device address of `scratch`, per device
+
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return PULSAR_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return PULSAR_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return PULSAR_EHIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return PULSAR_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G, const void* K,
+                        const void* V, int n_shards, int Tq, int64_t S, int Hq, int Hkv, int d,
+                        float softmax_scale, float* o, float* lse, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  const int chk = phase2_query_check(q, Kg, Vg, G, K, V, n_shards, Tq, S, Hq, Hkv, d,
+                                     softmax_scale, o);
+  if (chk != PULSAR_OK || Tq == 0) return chk;
   const size_t need = pulsar_phase2_query_workspace_bytes(n_shards, Tq, S, G, Hq, Hkv, d);
   if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
     return PULSAR_EWORKSPACE;
@@ -494,6 +536,22 @@ int pulsar_phase2_query(const void* q, const void* Kg, const void* Vg, int64_t G
   if (st != PULSAR_OK) return st;
   return launch_lse_merge(po, pl, parts, 1, Tq, Hq, d, ostride, lstride, o, lse,
                           (hipStream_t)stream);
+}
+
+int pulsar_phase2_query_noalloc(const void* q, const void* Kg, const void* Vg, int64_t G,
+                                const void* K, const void* V, int n_shards, int Tq, int64_t S,
+                                int Hq, int Hkv, int d, float softmax_scale, float* o, float* lse,
+                                void* stream) {
+  const int chk = phase2_query_check(q, Kg, Vg, G, K, V, n_shards, Tq, S, Hq, Hkv, d,
+                                     softmax_scale, o);
+  if (chk != PULSAR_OK || Tq == 0) return chk;
+  const size_t need = pulsar_phase2_query_workspace_bytes(n_shards, Tq, S, G, Hq, Hkv, d);
+  if (need > (size_t)PULSAR_STATIC_SCRATCH_BYTES) return PULSAR_ETOOLARGE;
+  void* ws = nullptr;
+  const int st = scratch_of_current_device(&ws);
+  if (st != PULSAR_OK) return st;
+  return pulsar_phase2_query(q, Kg, Vg, G, K, V, n_shards, Tq, S, Hq, Hkv, d, softmax_scale, o,
+                             lse, ws, (size_t)PULSAR_STATIC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"

@@ -196,6 +196,31 @@ def test_phase2_query_validation():
     assert lib.pulsar_phase2_workspace_bytes(0, 1, 512, 32, 8, 128) == 0
 
 
+def test_phase2_query_noalloc_validation():
+    # Host-side checks come before any device call: bad arguments, no work
+    # and partials beyond the static scratch all return without touching a GPU.
+    lib = _lib.lib()
+    f = lib.pulsar_phase2_query_noalloc
+    def call(q=FAKE, kg=FAKE, vg=FAKE, G=3, K=FAKE, V=FAKE, ns=4, Tq=8, S=1024, Hq=32, Hkv=8,
+             d=128, scale=0.088, o=FAKE):
+        return f(q, kg, vg, G, K, V, ns, Tq, S, Hq, Hkv, d, scale, o, None, None)
+    assert call(G=-1) == EINVAL
+    assert call(Hq=30) == EINVAL
+    assert call(scale=float("nan")) == EINVAL
+    assert call(kg=None) == EINVAL
+    assert call(o=FAKE + 4) == EINVAL
+    assert call(d=96) == EUNSUP
+    assert call(Tq=0) == 0
+    ETOOLARGE = -5
+    limit = 64 << 20
+    big = dict(ns=16, Tq=256, S=8192, G=0)
+    assert lib.pulsar_phase2_query_workspace_bytes(16, 256, 8192, 0, 32, 8, 128) > limit
+    assert call(**big) == ETOOLARGE
+    assert "scratch" in _lib.status_string(ETOOLARGE)
+    # the benchmark's 64-token query encoding over 16 shards fits
+    assert lib.pulsar_phase2_query_workspace_bytes(16, 64, 8192, 0, 32, 8, 128) <= limit
+
+
 def test_chunk_summaries_validation():
     f = _lib.lib().pulsar_chunk_summaries
     def call(ids=FAKE, batch=1, L=4096, N=4, m=16, k=4, V=1000, scorer=1, sel=FAKE):
