@@ -54,15 +54,20 @@ __device__ __forceinline__ void build_run_table(const RowMap& mp, const int32_t*
   }
 }
 
-// Global position of assembled row r.  Rows are below 2^24 (checked on the
-// host), so the float quotient estimate is within one of the true quotient.
-__device__ __forceinline__ int row_position(const RowMap& mp, const int* run_base, int r) {
-  if (mp.mode == MAP_IDENTITY) return (int)(mp.offset + r);
-  if (mp.mode == MAP_ANCHOR) return r < mp.Lb ? r : mp.block_idx * mp.Lb + (r - mp.Lb);
-  if (r < mp.sink) return r;
+// Global position of assembled row r, in two parts: the index of the LDS
+// run-table entry the row reads (-1 for none) and what to add to that entry
+// (or the position itself when there is no entry).  Rows are below 2^24
+// (checked on the host), so float quotient estimates are within one of the
+// true quotient.  MODE is the map mode, known at compile time.
+template <int MODE>
+__device__ __forceinline__ int2 row_position_split(const RowMap& mp, int r) {
+  if constexpr (MODE == MAP_IDENTITY) return int2{-1, (int)(mp.offset + r)};
+  if constexpr (MODE == MAP_ANCHOR)
+    return int2{-1, r < mp.Lb ? r : mp.block_idx * mp.Lb + (r - mp.Lb)};
+  if (r < mp.sink) return int2{-1, r};
   const int t = r - mp.sink;
-  if (t >= mp.prefix) return mp.block_idx * mp.Lb + (t - mp.prefix);
-  if (mp.mode == MAP_EVEN) {
+  if (t >= mp.prefix) return int2{-1, mp.block_idx * mp.Lb + (t - mp.prefix)};
+  if constexpr (MODE == MAP_EVEN) {
     // point p of block j: j*Lb + floor(p (Lb - 1) / (sigma - 1)); both
     // quotients are estimated in floating point and corrected exactly
     const int sig = mp.sigma;
@@ -75,13 +80,14 @@ __device__ __forceinline__ int row_position(const RowMap& mp, const int* run_bas
       ++j;
       p -= sig;
     }
-    if (sig == 1) return j * mp.Lb;
+    if (sig == 1) return int2{-1, j * mp.Lb};
     const int64_t num = (int64_t)p * (mp.Lb - 1);  // < 2^48: exact as a double
     int64_t off = (int64_t)((double)num * mp.inv_sigma1);
     if (off * (sig - 1) > num) --off;
     else if ((off + 1) * (sig - 1) <= num) ++off;
-    return j * mp.Lb + (int)off;
+    return int2{-1, j * mp.Lb + (int)off};
   }
+  // summary runs: run q starts at run_base[q]
   int q, w;
   if (mp.m_log2 >= 0) {
     q = t >> mp.m_log2;
@@ -97,7 +103,23 @@ __device__ __forceinline__ int row_position(const RowMap& mp, const int* run_bas
       w -= mp.chunk;
     }
   }
-  return run_base[q] + w;
+  return int2{q, w};
+}
+
+template <int MODE>
+__device__ __forceinline__ int row_position_m(const RowMap& mp, const int* run_base, int r) {
+  const int2 s = row_position_split<MODE>(mp, r);
+  return s.x >= 0 ? run_base[s.x] + s.y : s.y;
+}
+
+// The same with the mode read at run time.
+__device__ __forceinline__ int row_position(const RowMap& mp, const int* run_base, int r) {
+  switch (mp.mode) {
+    case MAP_IDENTITY: return row_position_m<MAP_IDENTITY>(mp, run_base, r);
+    case MAP_ANCHOR: return row_position_m<MAP_ANCHOR>(mp, run_base, r);
+    case MAP_EVEN: return row_position_m<MAP_EVEN>(mp, run_base, r);
+    default: return row_position_m<MAP_SUMMARY>(mp, run_base, r);
+  }
 }
 
 __device__ __forceinline__ float wave_max(float x) {
