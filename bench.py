@@ -141,6 +141,18 @@ def cpu_oracle_baseline(ids, q, k, v, sel_ref, cfg, n, budget_s=15.0):
     }
 
 
+def calibration_copy():
+    """A plain device copy of a known size (1 GiB read, 1 GiB write), far
+    larger than the caches: the scale for the FETCH_SIZE / WRITE_SIZE counters
+    of a rocprofv3 --pmc run of this command.  Returns the bytes copied."""
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    return src.numel() * 4
+
+
 IDF_THROUGHPUT_BATCH = 1024
 METRIC = "Phase-1 prefixed-block attn TFLOP/s (% bf16 MFMA peak); Max-IDF tokens/s"
 
@@ -194,6 +206,8 @@ def run_main(args):
     p1_ms = t_p1.mean_ms()
     p1_tflops = f_p1 / (p1_ms * 1e-3) / 1e12
     if args.profile_step:
+        if args.calibrate:
+            calibration_copy()
         print(json.dumps({"metric": METRIC, "value": p1_tflops, "unit": "TFLOP/s",
                           "ms_per_step": ms_step, "phase1_attn_ms": p1_ms,
                           "phase2_partial_merge_ms": t_p2.mean_ms(),
@@ -380,15 +394,7 @@ def run_main(args):
         },
     }
     if args.calibrate:
-        # a plain device copy of a known size (1 GiB read, 1 GiB write), far
-        # larger than the caches: the scale for the FETCH_SIZE / WRITE_SIZE
-        # counters of a rocprofv3 --pmc run of this command
-        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        result["calibration_copy_bytes"] = src.numel() * 4
+        result["calibration_copy_bytes"] = calibration_copy()
     if not args.no_cpu:
         from oracle import maxidf as oracle_maxidf
         sel_ref, _, _, _ = oracle_maxidf.maxidf_summaries(ids, N, cfg.chunk, cfg.topk, cfg.vocab)
