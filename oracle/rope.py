@@ -18,13 +18,27 @@ halves, and pair i < d/2, (x_i, x_{i+d/2}), is turned by the angle p * w_i,
 with w_i = base^(-2i/d) unless a frequency table is given (a model's scaled
 table, e.g. Llama-3.1's, is passed as that table).
 
+The same appendix describes a contiguous mode (unused in the paper's
+experiments): block i's assembled input is renumbered 0 .. n_i - 1 for its
+Phase-1 pass, and the Phase-2 query positions start just past the longest
+assembled Phase-1 input.  In sparse mode a query keeps its place after the
+whole context.
+
 Readings: the paper names neither the rotary form nor its base; the
 rotate-half form and a caller-given base or table follow the evaluated
-models.  Everything is fp64 on inputs already rounded to bf16.
+models.  "Just past the longest assembled Phase-1 length" is read as: the
+first query (or generated) token after the context has position
+max_i n_i, the next one max_i n_i + 1, and so on.  Everything is fp64 on
+inputs already rounded to bf16.
 """
 from __future__ import annotations
 
 import numpy as np
+
+from . import assembly
+
+SPARSE = 0
+CONTIGUOUS = 1
 
 
 def inv_freq(d: int, base: float) -> np.ndarray:
@@ -51,3 +65,36 @@ def rope(x, pos, freqs) -> np.ndarray:
     c, s = np.cos(ang), np.sin(ang)
     lo, hi = x[..., : d // 2], x[..., d // 2:]
     return np.concatenate([lo * c - hi * s, hi * c + lo * s], axis=-1)
+
+
+def phase1_rope_positions(L: int, num_blocks: int, block_idx: int, sink: int, chunk: int,
+                          topk: int, sel_seq=None, prefix_mode: int = assembly.PREFIX_SUMMARY,
+                          pos_mode: int = SPARSE) -> np.ndarray:
+    """Rotary position of every row of block i's assembled Phase-1 input:
+    its global position (sparse) or its row index (contiguous)."""
+    if pos_mode == SPARSE:
+        return assembly.phase1_positions(L, num_blocks, block_idx, sink, chunk, topk, sel_seq,
+                                         prefix_mode)
+    n = assembly.phase1_len(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode)
+    return np.arange(n, dtype=np.int64)
+
+
+def query_positions(L: int, num_blocks: int, sink: int, chunk: int, topk: int, Tq: int,
+                    G: int = 0, prefix_mode: int = assembly.PREFIX_SUMMARY,
+                    pos_mode: int = SPARSE) -> np.ndarray:
+    """Rotary positions of Tq Phase-2 tokens that follow G earlier query or
+    generated tokens: after the context (sparse), or after the longest
+    assembled Phase-1 input (contiguous)."""
+    if pos_mode == SPARSE:
+        first = L
+    else:
+        first = max(assembly.phase1_len(L, num_blocks, i, sink, chunk, topk, prefix_mode)
+                    for i in range(num_blocks))
+    return first + G + np.arange(Tq, dtype=np.int64)
+
+
+def assembled_rope(x, src_pos, rot_pos, freqs) -> np.ndarray:
+    """Rows of a per-position tensor x [L, H, d] at the global positions
+    src_pos, each rotated by its entry of rot_pos (fp64)."""
+    rows = np.asarray(x, dtype=np.float64)[np.asarray(src_pos, dtype=np.int64)]
+    return rope(rows, np.asarray(rot_pos), freqs)

@@ -96,3 +96,81 @@ def test_sparse_positions_are_the_global_rotation_gathered():
     pos = assembly.phase1_positions(L, nb, 3, sink, chunk, k, sel)
     whole = rope.rope(x, np.arange(L), w)
     assert np.array_equal(rope.rope(x[pos], pos, w), whole[pos])
+
+
+# ------------------------------------------------------------ contiguous mode --
+# Appendix "RoPE Position ID Assignment", contiguous: block i's assembled input
+# is renumbered 0 .. n_i - 1 and Phase-2 positions start just past the longest
+# assembled input.
+
+def test_contiguous_positions_hand_example():
+    # L = 64, 4 blocks of 16, sink 2, chunk 2, top-1: block 3's input is
+    # [sink 0 1 | Sigma_0 | Sigma_1 | Sigma_2 | B_3] with 2 + 3*2 + 16 = 24 rows
+    sel = np.array([[5], [0], [7], [3]])
+    sp = rope.phase1_rope_positions(64, 4, 3, 2, 2, 1, sel, pos_mode=rope.SPARSE)
+    assert sp.tolist() == [0, 1, 10, 11, 16, 17, 46, 47] + list(range(48, 64))
+    ct = rope.phase1_rope_positions(64, 4, 3, 2, 2, 1, sel, pos_mode=rope.CONTIGUOUS)
+    assert ct.tolist() == list(range(24))
+    # the longest input is block 3's: 24 rows, so queries start at 24
+    q = rope.query_positions(64, 4, 2, 2, 1, Tq=3, pos_mode=rope.CONTIGUOUS)
+    assert q.tolist() == [24, 25, 26]
+    # sparse queries follow the 64-token context; G earlier tokens shift them
+    assert rope.query_positions(64, 4, 2, 2, 1, Tq=2, G=5).tolist() == [69, 70]
+    assert rope.query_positions(64, 4, 2, 2, 1, Tq=1, G=5,
+                                pos_mode=rope.CONTIGUOUS).tolist() == [29]
+
+
+@pytest.mark.parametrize("mode", [assembly.PREFIX_SUMMARY, assembly.PREFIX_ANCHOR,
+                                  assembly.PREFIX_EVEN])
+def test_contiguous_block0_equals_sparse_and_queries_come_after_every_row(mode):
+    # Input_0 = [B_0] sits at global positions 0 .. Lb-1: both modes agree.
+    # Contiguous queries come after every row of every block's input, and the
+    # first one directly after the longest input.
+    rng = np.random.default_rng(3)
+    L, N, s, m, k = 512, 8, 8, 4, 3
+    sel = np.stack([np.sort(rng.choice(L // N // m, k, replace=False)) for _ in range(N)])
+    a = rope.phase1_rope_positions(L, N, 0, s, m, k, sel, mode, rope.SPARSE)
+    b = rope.phase1_rope_positions(L, N, 0, s, m, k, sel, mode, rope.CONTIGUOUS)
+    assert np.array_equal(a, b)
+    q = rope.query_positions(L, N, s, m, k, Tq=4, prefix_mode=mode, pos_mode=rope.CONTIGUOUS)
+    last = max(rope.phase1_rope_positions(L, N, i, s, m, k, sel, mode, rope.CONTIGUOUS).max()
+               for i in range(N))
+    assert q[0] == last + 1
+    if mode == assembly.PREFIX_ANCHOR:
+        assert q[0] == 2 * (L // N)          # Star-style [B_0 || B_i], 2 Lb rows
+
+
+def test_contiguous_keeps_distances_inside_b_i_only():
+    # Rotated scores depend on position differences.  Within B_i the rows are
+    # consecutive in both modes, so scores between them agree; a summary row
+    # is k*m*(i-1-j)+... rows away in contiguous mode but blocks away in
+    # sparse mode, so its scores against B_i differ.
+    rng = np.random.default_rng(11)
+    L, N, s, m, k, H, d = 256, 4, 4, 4, 2, 1, 16
+    sel = np.stack([np.sort(rng.choice(L // N // m, k, replace=False)) for _ in range(N)])
+    x = rng.standard_normal((L, H, d))
+    w = rope.inv_freq(d, 10000.0)
+    src = assembly.phase1_positions(L, N, 3, s, m, k, sel)
+    sp = rope.assembled_rope(x, src, rope.phase1_rope_positions(L, N, 3, s, m, k, sel), w)
+    ct = rope.assembled_rope(x, src, rope.phase1_rope_positions(L, N, 3, s, m, k, sel,
+                                                                pos_mode=rope.CONTIGUOUS), w)
+    n, Lb = len(src), L // N
+    bi = np.arange(n - Lb, n)
+    g_sp = np.einsum("rhd,chd->rc", sp[bi], sp[bi])
+    g_ct = np.einsum("rhd,chd->rc", ct[bi], ct[bi])
+    np.testing.assert_allclose(g_sp, g_ct, atol=1e-9)
+    summ = s  # first summary row
+    c_sp = np.einsum("rhd,hd->r", sp[bi], sp[summ])
+    c_ct = np.einsum("rhd,hd->r", ct[bi], ct[summ])
+    assert np.max(np.abs(c_sp - c_ct)) > 1e-3
+
+
+def test_assembled_rope_turns_each_row_by_its_own_position():
+    # d = 2, w = 1: row r of (1, 0) rows, gathered from any positions and
+    # rotated contiguously, is (cos r, sin r)
+    x = np.zeros((10, 1, 2))
+    x[:, 0, 0] = 1.0
+    src = np.array([7, 2, 2, 9])
+    y = rope.assembled_rope(x, src, np.arange(4), np.array([1.0]))
+    for r in range(4):
+        assert np.allclose(y[r, 0], [math.cos(r), math.sin(r)], atol=1e-15)
