@@ -54,6 +54,14 @@ typedef enum {
 
 typedef enum { PULSAR_OUT_F32 = 0, PULSAR_OUT_BF16 = 1 } pulsar_out_dtype;
 
+/* Rotary position ids of an assembled Phase-1 input (Appendix "RoPE Position
+   ID Assignment"). */
+typedef enum {
+  PULSAR_POS_SPARSE = 0,      /* every row keeps its global position (the paper's default) */
+  PULSAR_POS_CONTIGUOUS = 1,  /* block i's input renumbered 0 .. n_i - 1 */
+  PULSAR_POS_NONE = 2         /* no rotation (values) */
+} pulsar_pos_mode;
+
 /* Chunk scorers (Appendix "Scoring Heuristic Details"). */
 typedef enum {
   PULSAR_SCORE_MAXIDF = 0,  /* max over the chunk of IDF (Eq. maxidf) */
@@ -176,6 +184,40 @@ int64_t pulsar_phase1_len(int64_t L, int num_blocks, int block_idx, int sink, in
 int pulsar_phase1_positions(const int32_t* sel_chunks, int batch, int64_t L, int num_blocks,
                             int block_idx, int sink, int chunk, int topk, int prefix_mode,
                             int32_t* pos, void* stream);
+
+/*
+ * Block i's assembled Phase-1 input materialised with rotary position
+ * embedding (Eq. 3; Appendix "RoPE Position ID Assignment").
+ *
+ * Row r of X_out is the row of X at the global position of assembled row r
+ * (the map of pulsar_phase1_positions), rotated in the rotate-half form of
+ * pulsar_rope by
+ *   PULSAR_POS_SPARSE      its global position (the same rows as rotating X
+ *                          once with pulsar_rope and gathering),
+ *   PULSAR_POS_CONTIGUOUS  r: the input renumbered 0 .. n_i - 1,
+ *   PULSAR_POS_NONE        nothing (a plain gather, for V).
+ * Contiguous mode changes a row's rotation with the block whose input it
+ * enters, so each block's Q and K are materialised this way; attention over
+ * them is pulsar_phase1_attn on X_out with num_blocks = 1, block_idx = 0 and
+ * L = n_i (the identity map), whose last Lb rows of K/V are the retained
+ * KV(B_i).  Phase-2 tokens then take positions from max_i n_i on
+ * (pulsar_rope with pos = NULL and pos_offset = max_i n_i + the number of
+ * earlier Phase-2 tokens).
+ *
+ * X         bf16 [batch, L, H, d], 16-byte aligned, not modified.
+ * sel_chunks as for pulsar_phase1_positions.
+ * inv_freq  HOST pointer to d/2 frequencies, or NULL for base^(-2i/d)
+ *           (ignored with PULSAR_POS_NONE).
+ * X_out     out bf16 [batch, n_i, H, d], 16-byte aligned.
+ * EINVAL: as pulsar_phase1_len, batch < 0, H < 1, unknown pos_mode, NULL or
+ *         misaligned X / X_out when there is work, NULL sel_chunks when
+ *         needed, odd d, a non-finite table entry or base, L >= 2^31.
+ * EUNSUPPORTED: d not in {64, 128}; n_i >= 2^24.
+ */
+int pulsar_phase1_gather(const void* X, int batch, int64_t L, int H, int d, int num_blocks,
+                         int block_idx, int sink, int chunk, int topk, const int32_t* sel_chunks,
+                         int prefix_mode, int pos_mode, const float* inv_freq, double base,
+                         void* X_out, void* stream);
 
 /*
  * Phase-1 prefixed-block causal attention (Algorithm 1, forward pass of

@@ -24,6 +24,9 @@ SIGNATURES = {
     "pulsar_phase1_len": (_c_i64, [_c_i64, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),
     "pulsar_phase1_positions": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
                                          _c_int, _c_int, _vp, _vp]),
+    "pulsar_phase1_gather": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int, _c_int,
+                                      _c_int, _c_int, _vp, _c_int, _c_int, _vp, ctypes.c_double,
+                                      _vp, _vp]),
     "pulsar_phase1_attn": (_c_int, [_vp, _vp, _vp, _c_int, _c_i64, _c_int, _c_int, _c_int,
                                     _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _c_int,
                                     _c_float, _vp, _c_int, _vp, _vp, _vp, _vp]),

@@ -18,6 +18,9 @@ PREFIX_ANCHOR = 1
 PREFIX_EVEN = 2
 OUT_F32 = 0
 OUT_BF16 = 1
+POS_SPARSE = 0
+POS_CONTIGUOUS = 1
+POS_NONE = 2
 SCORE_MAXIDF = 0
 SCORE_TFIDF = 1
 SCORE_BM25 = 2
@@ -105,6 +108,37 @@ def phase1_positions(sel, batch: int, L: int, num_blocks: int, block_idx: int, s
                                             chunk, topk, prefix_mode, _ptr(pos), _stream())
     _lib.check(st, "pulsar_phase1_positions")
     return pos
+
+
+def _freq_table(inv_freq, d):
+    if inv_freq is None:
+        return None
+    vals = [float(v) for v in (inv_freq.tolist() if hasattr(inv_freq, "tolist") else inv_freq)]
+    if len(vals) != d // 2:
+        raise ValueError("inv_freq must hold d/2 values")
+    return (ctypes.c_float * len(vals))(*vals)
+
+
+def phase1_gather(X, num_blocks: int, block_idx: int, sink: int, chunk: int, topk: int,
+                  sel=None, prefix_mode: int = PREFIX_SUMMARY, pos_mode: int = POS_SPARSE,
+                  inv_freq=None, base: float = 500000.0):
+    """Block i's assembled input from X bf16 [b, L, H, d], each row rotated
+    by its global position (POS_SPARSE), its row index (POS_CONTIGUOUS) or not
+    at all (POS_NONE) -> bf16 [b, n_i, H, d]."""
+    _need(X, torch.bfloat16, "X")
+    if sel is not None:
+        _need(sel, torch.int32, "sel")
+    b, L, H, d = X.shape
+    n = phase1_len(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode)
+    out = torch.empty((b, n, H, d), dtype=torch.bfloat16, device=X.device)
+    table = _freq_table(inv_freq, d)
+    st = _lib.lib().pulsar_phase1_gather(_ptr(X), b, L, H, d, num_blocks, block_idx, sink, chunk,
+                                         topk, _ptr(sel), prefix_mode, pos_mode,
+                                         None if table is None else
+                                         ctypes.cast(table, ctypes.c_void_p),
+                                         float(base), _ptr(out), _stream())
+    _lib.check(st, "pulsar_phase1_gather")
+    return out
 
 
 def phase1_attn(Q, K, V, num_blocks: int, block_idx: int, sink: int, chunk: int, topk: int,
@@ -205,12 +239,7 @@ def rope_(x, pos=None, pos_offset: int = 0, inv_freq=None, base: float = 500000.
         _need(pos, torch.int32, "pos")
         if pos.numel() != batch * n:
             raise ValueError("pos must hold one position per row")
-    table = None
-    if inv_freq is not None:
-        vals = [float(v) for v in (inv_freq.tolist() if hasattr(inv_freq, "tolist") else inv_freq)]
-        if len(vals) != d // 2:
-            raise ValueError("inv_freq must hold d/2 values")
-        table = (ctypes.c_float * len(vals))(*vals)
+    table = _freq_table(inv_freq, d)
     st = _lib.lib().pulsar_rope(_ptr(xv), batch, n, H, d, _ptr(pos), int(pos_offset),
                                 None if table is None else ctypes.cast(table, ctypes.c_void_p),
                                 float(base), _stream())

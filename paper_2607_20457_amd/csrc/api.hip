@@ -8,7 +8,7 @@
 
 namespace {
 
-constexpr int kVersion = 3;
+constexpr int kVersion = 4;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -149,6 +149,28 @@ int pulsar_phase1_positions(const int32_t* sel_chunks, int batch, int64_t L, int
   const int32_t* sel = needs_sel(block_idx, topk, prefix_mode) ? sel_chunks : nullptr;
   return launch_positions(mp, sel, (int64_t)num_blocks * topk, batch, (int)n, pos,
                           (hipStream_t)stream);
+}
+
+int pulsar_phase1_gather(const void* X, int batch, int64_t L, int H, int d, int num_blocks,
+                         int block_idx, int sink, int chunk, int topk, const int32_t* sel_chunks,
+                         int prefix_mode, int pos_mode, const float* inv_freq, double base,
+                         void* X_out, void* stream) {
+  const int64_t n = phase1_len_checked(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  if (n < 0) return (int)n;
+  if (batch < 0 || H < 1 || d < 1 || L >= ((int64_t)1 << 31)) return PULSAR_EINVAL;
+  if (pos_mode != PULSAR_POS_SPARSE && pos_mode != PULSAR_POS_CONTIGUOUS &&
+      pos_mode != PULSAR_POS_NONE)
+    return PULSAR_EINVAL;
+  if (d != 64 && d != 128) return d % 2 == 0 ? PULSAR_EUNSUPPORTED : PULSAR_EINVAL;
+  if (n >= PULSAR_MAX_ROWS) return PULSAR_EUNSUPPORTED;
+  if (batch == 0 || n == 0) return PULSAR_OK;
+  if (X == nullptr || X_out == nullptr || !aligned16(X) || !aligned16(X_out)) return PULSAR_EINVAL;
+  if (needs_sel(block_idx, topk, prefix_mode) && sel_chunks == nullptr) return PULSAR_EINVAL;
+  const RowMap mp = make_map(L, num_blocks, block_idx, sink, chunk, topk, prefix_mode);
+  const int32_t* sel = needs_sel(block_idx, topk, prefix_mode) ? sel_chunks : nullptr;
+  return launch_gather_rope(static_cast<const uint16_t*>(X), static_cast<uint16_t*>(X_out), batch,
+                            (int)n, L, H, d, mp, sel, (int64_t)num_blocks * topk, pos_mode,
+                            inv_freq, base, (hipStream_t)stream);
 }
 
 int pulsar_phase1_attn(const void* Q, const void* K, const void* V, int batch, int64_t L, int Hq,

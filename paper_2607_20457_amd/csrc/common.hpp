@@ -203,6 +203,12 @@ int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz
                      int d, int64_t part_ostride, int64_t part_lstride, float* o, float* lse,
                      hipStream_t stream);
 
+// Rows of an assembled Phase-1 input gathered from a per-position tensor and
+// rotated per pos_mode (a pulsar_pos_mode).
+int launch_gather_rope(const uint16_t* X, uint16_t* Y, int batch, int n, int64_t L, int H, int d,
+                       const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int pos_mode,
+                       const float* inv_freq, double base, hipStream_t stream);
+
 // IDF of a context with no tokens: every entry ln(num_blocks / 1).
 int launch_idf_fill(float* idf, int64_t n, int num_blocks, hipStream_t stream);
 

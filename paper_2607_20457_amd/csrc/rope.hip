@@ -37,19 +37,17 @@ constexpr double kTwoPiHi = 6.283185307179586;
 constexpr double kTwoPiLo = 2.4492935982947064e-16;
 constexpr double kInvTwoPi = 0.15915494309189535;
 
-template <int D, bool HAS_POS>
-__global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict__ X,
-                                                            int64_t rows, int64_t n_rows, int H,
-                                                            const int32_t* __restrict__ pos,
-                                                            int64_t pos_offset, RopeFreqs f) {
+// One row of H heads: 16-byte loads of src (already offset by this lane's
+// 8 pairs), rotation by the angles of position p + p_add (ROTATE) or a plain
+// copy, 16-byte stores to dst.  `w_pair` and `p` may still be loading: the
+// first data is requested before they are used.
+template <int D, bool ROTATE>
+__device__ __forceinline__ void rope_row(const uint16_t* src, uint16_t* dst, int H, int64_t p,
+                                         int64_t p_add, double w_pair, int lane) {
   constexpr int G = D / 16;     // lanes per head: pairs 8j .. 8j+7 each
   constexpr int HPW = 64 / G;   // heads per wavefront step
   constexpr int U = 4;          // steps whose loads are in flight together
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * (kRopeThreads / 64) + (threadIdx.x >> 6);
-  if (row >= rows) return;  // wave-uniform
   const int j = lane % G, hl = lane / G;
-  uint16_t* base = X + row * (int64_t)H * D + 8 * j;
   // Heads hl, hl + HPW, ...: one step covers HPW heads of the row, its low
   // and high halves as two runs of contiguous 16-byte chunks.  Loads are
   // branch-free (a head past the last re-reads the last; it is not stored).
@@ -58,33 +56,31 @@ __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int hh = min(h0 + u * HPW + hl, H - 1);
-      lo[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D);
-      hi[u] = *reinterpret_cast<const u32x4*>(base + (int64_t)hh * D + D / 2);
+      lo[u] = *reinterpret_cast<const u32x4*>(src + (int64_t)hh * D);
+      hi[u] = *reinterpret_cast<const u32x4*>(src + (int64_t)hh * D + D / 2);
     }
   };
   // The row's angles: lane (hl, j) forms that of pair 8j + hl % 8, then
   // each lane gathers the eight of its own pairs 8j .. 8j+7 from lanes
-  // v * G + j.  The frequency and the position are requested before the
-  // first data, which then stays in flight while the angle is formed.
-  const int pair = 8 * j + (hl & 7);
-  double w = f.w[pair];
-  int64_t p = HAS_POS ? (int64_t)pos[row] : row % n_rows;
+  // v * G + j.
   load(0);
-  asm volatile("" : "+v"(w), "+v"(p));
-  p += pos_offset;
-  float s1, c1;
-  {
-    const double a = (double)p * w;
-    const double k = rint(a * kInvTwoPi);
-    double r = fma(-k, kTwoPiHi, a);
-    r = fma(-k, kTwoPiLo, r);
-    sincosf((float)r, &s1, &c1);
-  }
   float c[8], s[8];
+  if constexpr (ROTATE) {
+    asm volatile("" : "+v"(w_pair), "+v"(p));
+    p += p_add;
+    float s1, c1;
+    {
+      const double a = (double)p * w_pair;
+      const double k = rint(a * kInvTwoPi);
+      double r = fma(-k, kTwoPiHi, a);
+      r = fma(-k, kTwoPiLo, r);
+      sincosf((float)r, &s1, &c1);
+    }
 #pragma unroll
-  for (int v = 0; v < 8; ++v) {
-    s[v] = __shfl(s1, v * G + j, 64);
-    c[v] = __shfl(c1, v * G + j, 64);
+    for (int v = 0; v < 8; ++v) {
+      s[v] = __shfl(s1, v * G + j, 64);
+      c[v] = __shfl(c1, v * G + j, 64);
+    }
   }
   auto rotate = [&](const u32x4 lo, const u32x4 hi, u32x4& olo, u32x4& ohi) {
 #pragma unroll
@@ -113,16 +109,111 @@ __global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict
     for (int u = 0; u < U; ++u) {
       const int hh = h0 + u * HPW + hl;
       if (hh < H) {
-        u32x4 olo, ohi;
-        rotate(clo[u], chi[u], olo, ohi);
-        *reinterpret_cast<u32x4*>(base + (int64_t)hh * D) = olo;
-        *reinterpret_cast<u32x4*>(base + (int64_t)hh * D + D / 2) = ohi;
+        u32x4 olo = clo[u], ohi = chi[u];
+        if constexpr (ROTATE) rotate(clo[u], chi[u], olo, ohi);
+        *reinterpret_cast<u32x4*>(dst + (int64_t)hh * D) = olo;
+        *reinterpret_cast<u32x4*>(dst + (int64_t)hh * D + D / 2) = ohi;
       }
     }
   }
 }
 
+template <int D, bool HAS_POS>
+__global__ __launch_bounds__(kRopeThreads) void rope_kernel(uint16_t* __restrict__ X,
+                                                            int64_t rows, int64_t n_rows, int H,
+                                                            const int32_t* __restrict__ pos,
+                                                            int64_t pos_offset, RopeFreqs f) {
+  constexpr int G = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * (kRopeThreads / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;  // wave-uniform
+  const int j = lane % G, hl = lane / G;
+  uint16_t* base = X + row * (int64_t)H * D + 8 * j;
+  // The frequency and the position are requested before the first data.
+  const double w = f.w[8 * j + (hl & 7)];
+  const int64_t p = HAS_POS ? (int64_t)pos[row] : row % n_rows;
+  rope_row<D, true>(base, base, H, p, pos_offset, w, lane);
+}
+
+// Rows of block i's assembled Phase-1 input (Eq. 3), gathered from the
+// per-position tensor X through the row -> position map and rotated by
+// their global position (ROT = 1, sparse), by their row index (ROT = 2,
+// contiguous), or copied unrotated (ROT = 0, for V).  One wavefront per
+// output row; its position is formed by the whole wave (the selection entry
+// of a summary row is one read from sel, clamped into the block as the
+// attention kernel's run table does).
+template <int D, int ROT>
+__global__ __launch_bounds__(kRopeThreads) void gather_rope_kernel(
+    const uint16_t* __restrict__ X, uint16_t* __restrict__ Y, int64_t rows, int n,
+    int64_t x_bstride, int H, RowMap mp, const int32_t* __restrict__ sel, int64_t sel_bstride,
+    RopeFreqs f) {
+  constexpr int G = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * (kRopeThreads / 64) + (threadIdx.x >> 6);
+  if (row >= rows) return;  // wave-uniform
+  const int64_t b = row / n;
+  const int r = (int)(row - b * n);
+  int2 ps;
+  switch (mp.mode) {
+    case MAP_IDENTITY: ps = row_position_split<MAP_IDENTITY>(mp, r); break;
+    case MAP_ANCHOR: ps = row_position_split<MAP_ANCHOR>(mp, r); break;
+    case MAP_EVEN: ps = row_position_split<MAP_EVEN>(mp, r); break;
+    default: ps = row_position_split<MAP_SUMMARY>(mp, r); break;
+  }
+  int p = ps.y;
+  if (ps.x >= 0) {  // summary run q = ps.x: block q / k, chunk sel[q]
+    const int q = ps.x;
+    const int c = min(max(sel[b * sel_bstride + q], 0), mp.nchunk - 1);
+    p = (q / mp.topk) * mp.Lb + c * mp.chunk + ps.y;
+  }
+  const int j = lane % G, hl = lane / G;
+  const uint16_t* src = X + b * x_bstride + (int64_t)p * H * D + 8 * j;
+  uint16_t* dst = Y + row * (int64_t)H * D + 8 * j;
+  const double w = f.w[8 * j + (hl & 7)];
+  rope_row<D, ROT != 0>(src, dst, H, ROT == 2 ? (int64_t)r : (int64_t)p, 0, w, lane);
+}
+
+// The table w_i: the caller's (checked finite) or base^(-2i/d).
+int make_freqs(const float* inv_freq, double base, int d, RopeFreqs* f) {
+  if (inv_freq) {
+    for (int i = 0; i < d / 2; ++i) {
+      if (!std::isfinite(inv_freq[i])) return PULSAR_EINVAL;
+      f->w[i] = (double)inv_freq[i];
+    }
+  } else {
+    if (!(base > 0.0) || !std::isfinite(base)) return PULSAR_EINVAL;
+    for (int i = 0; i < d / 2; ++i) f->w[i] = std::pow(base, -2.0 * i / d);
+  }
+  return PULSAR_OK;
+}
+
 }  // namespace
+
+int launch_gather_rope(const uint16_t* X, uint16_t* Y, int batch, int n, int64_t L, int H, int d,
+                       const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int pos_mode,
+                       const float* inv_freq, double base, hipStream_t stream) {
+  RopeFreqs f{};
+  if (pos_mode != PULSAR_POS_NONE) {
+    const int st = make_freqs(inv_freq, base, d, &f);
+    if (st != PULSAR_OK) return st;
+  }
+  const int64_t rows = (int64_t)batch * n;
+  if (rows == 0 || H == 0) return PULSAR_OK;
+  const int64_t blocks = (rows + kRopeThreads / 64 - 1) / (kRopeThreads / 64);  // a wave per row
+  if (blocks > 0x7fffffff) return PULSAR_EUNSUPPORTED;
+  decltype(&gather_rope_kernel<128, 0>) kern;
+  if (d == 128)
+    kern = pos_mode == PULSAR_POS_SPARSE       ? gather_rope_kernel<128, 1>
+           : pos_mode == PULSAR_POS_CONTIGUOUS ? gather_rope_kernel<128, 2>
+                                               : gather_rope_kernel<128, 0>;
+  else
+    kern = pos_mode == PULSAR_POS_SPARSE       ? gather_rope_kernel<64, 1>
+           : pos_mode == PULSAR_POS_CONTIGUOUS ? gather_rope_kernel<64, 2>
+                                               : gather_rope_kernel<64, 0>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kRopeThreads), 0, stream, X, Y, rows, n,
+                     L * H * d, H, mp, sel, sel_bstride, f);
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
 
 extern "C" {
 
@@ -134,15 +225,8 @@ int pulsar_rope(void* X, int batch, int64_t n_rows, int H, int d, const int32_t*
   if (rows == 0 || H == 0) return PULSAR_OK;
   if (X == nullptr || (reinterpret_cast<uintptr_t>(X) & 15u) != 0) return PULSAR_EINVAL;
   RopeFreqs f{};
-  if (inv_freq) {
-    for (int i = 0; i < d / 2; ++i) {
-      if (!std::isfinite(inv_freq[i])) return PULSAR_EINVAL;
-      f.w[i] = (double)inv_freq[i];
-    }
-  } else {
-    if (!(base > 0.0) || !std::isfinite(base)) return PULSAR_EINVAL;
-    for (int i = 0; i < d / 2; ++i) f.w[i] = std::pow(base, -2.0 * i / d);
-  }
+  const int fst = make_freqs(inv_freq, base, d, &f);
+  if (fst != PULSAR_OK) return fst;
   const int64_t blocks = (rows + kRopeThreads / 64 - 1) / (kRopeThreads / 64);  // a wave per row
   if (blocks > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   auto s = (hipStream_t)stream;

@@ -221,6 +221,23 @@ def test_phase2_query_noalloc_validation():
     assert lib.pulsar_phase2_query_workspace_bytes(16, 64, 8192, 0, 32, 8, 128) <= limit
 
 
+def test_phase1_gather_validation():
+    f = _lib.lib().pulsar_phase1_gather
+    def call(X=FAKE, batch=1, L=4096, H=2, d=64, N=4, i=2, s=64, m=16, k=4, sel=FAKE, mode=0,
+             pm=1, base=10000.0, out=FAKE):
+        return f(X, batch, L, H, d, N, i, s, m, k, sel, mode, pm, None, base, out, None)
+    assert call(pm=3) == EINVAL and call(pm=-1) == EINVAL
+    assert call(L=4097) == EINVAL
+    assert call(i=4) == EINVAL
+    assert call(H=0) == EINVAL
+    assert call(X=None) == EINVAL and call(out=None) == EINVAL
+    assert call(out=FAKE + 2) == EINVAL
+    assert call(sel=None) == EINVAL                  # summary mode needs a selection
+    assert call(base=0.0) == EINVAL                  # rotating needs a base or table
+    assert call(d=96) == EUNSUP and call(d=63) == EINVAL
+    assert call(batch=0, X=None, out=None) == 0      # nothing to do
+
+
 def test_chunk_summaries_validation():
     f = _lib.lib().pulsar_chunk_summaries
     def call(ids=FAKE, batch=1, L=4096, N=4, m=16, k=4, V=1000, scorer=1, sel=FAKE):

@@ -127,3 +127,115 @@ def test_rope_empty_and_position_zero():
     X = to_dev_bf16(x)
     P.rope_(X)  # row 0: position 0, the identity
     assert np.array_equal(_bits(X), x.view(np.uint16))
+
+
+# ------------------------------------------------ assembled inputs, contiguous --
+
+def _gather_case(cfg, i, mode, batch=2, seed=5):
+    x = workload.bf16_normal(seed, (batch, cfg.L, cfg.Hkv, cfg.d))
+    rng = np.random.default_rng(seed)
+    C = cfg.Lb // cfg.chunk
+    sel = np.stack([np.stack([np.sort(rng.choice(C, cfg.topk, replace=False))
+                              for _ in range(cfg.num_blocks)]) for _ in range(batch)])
+    return x, sel.astype(np.int32)
+
+
+GATHER_CASES = [
+    workload.Config("g_tiny", L=4096, vocab=1, num_blocks=4, sink=64, chunk=16, topk=4,
+                    Hq=4, Hkv=3, d=64),
+    workload.Config("g_ragged", L=4000, vocab=1, num_blocks=4, sink=40, chunk=20, topk=3,
+                    Hq=8, Hkv=5, d=128),
+    workload.Config("g_128k", L=131072, vocab=1, num_blocks=16, sink=64, chunk=32, topk=32,
+                    Hq=32, Hkv=8, d=128),
+]
+
+
+@pytest.mark.parametrize("cfg", GATHER_CASES, ids=lambda c: c.name)
+@pytest.mark.parametrize("mode", [P.PREFIX_SUMMARY, P.PREFIX_ANCHOR, P.PREFIX_EVEN])
+def test_gather_contiguous_sparse_and_plain(cfg, mode):
+    i = cfg.num_blocks - 1
+    batch = 1 if cfg.L > 100000 else 2
+    x, sel = _gather_case(cfg, i, mode, batch)
+    X, S = to_dev_bf16(x), to_dev_i32(sel)
+    print(f"gather: {cfg.name} block {i} mode {mode} batch {batch}", flush=True)
+    w = orope.inv_freq(cfg.d, 500000.0)
+    plain = P.phase1_gather(X, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S, mode,
+                            P.POS_NONE)
+    sparse = P.phase1_gather(X, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S, mode,
+                             P.POS_SPARSE)
+    cont = P.phase1_gather(X, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S, mode,
+                           P.POS_CONTIGUOUS)
+    whole = X.clone()
+    P.rope_(whole)                                   # sparse: rotate once, then gather
+    torch.cuda.synchronize()
+    for b in range(batch):
+        sel_b = None if mode != P.PREFIX_SUMMARY else sel[b]
+        pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk,
+                                        sel_b, mode)
+        assert np.array_equal(_bits(plain[b]), x[b][pos])                 # bit-exact gather
+        assert np.array_equal(_bits(sparse[b]), _bits(whole[b])[pos])    # same rotation code
+        rows = np.unique(np.concatenate([np.arange(min(200, len(pos))),
+                                         np.linspace(0, len(pos) - 1, 300).astype(int)]))
+        rot = orope.phase1_rope_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk,
+                                          cfg.topk, sel_b, mode, orope.CONTIGUOUS)
+        xr = f64(x[b][pos[rows]])                    # the sampled rows' inputs
+        idx = np.arange(len(rows))
+        ref = orope.assembled_rope(xr, idx, rot[rows], w)
+        check_rounding(_bits(cont[b])[rows], ref, xr, f"{cfg.name} mode {mode} contiguous")
+        ref = orope.assembled_rope(xr, idx, pos[rows], w)
+        check_rounding(_bits(sparse[b])[rows], ref, xr, f"{cfg.name} mode {mode} sparse")
+
+
+def _round_bf16(a):
+    """fp64 -> bf16 (nearest-even through fp32), back as fp64."""
+    b = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def test_contiguous_phase1_and_phase2_positions_end_to_end():
+    # Contiguous mode (Appendix "RoPE Position ID Assignment"): block i's
+    # input renumbered 0..n_i-1, attention over the materialised rows (the
+    # identity map), and Phase-2 queries from max_i n_i on.  The oracle rotates
+    # in fp64 and rounds the rotated rows to bf16, the precision the
+    # materialised rows have.
+    from oracle import attention
+    cfg = workload.CONFIGS["tiny"]
+    q, k, v = workload.make_qkv(cfg)
+    ids = workload.make_ids(cfg)
+    from oracle import maxidf
+    sel, _, _, _ = maxidf.maxidf_summaries(ids, cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab)
+    Q, K, V, S = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), to_dev_i32(sel)
+    w = orope.inv_freq(cfg.d, 500000.0)
+    scale = 1 / math.sqrt(cfg.d)
+    for i in (1, cfg.num_blocks - 1):
+        args = (cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S, P.PREFIX_SUMMARY)
+        Qc = P.phase1_gather(Q, *args, P.POS_CONTIGUOUS)
+        Kc = P.phase1_gather(K, *args, P.POS_CONTIGUOUS)
+        Vc = P.phase1_gather(V, *args, P.POS_NONE)
+        n = Qc.shape[1]
+        o, lse = P.phase1_attn(Qc, Kc, Vc, 1, 0, 0, cfg.chunk, 0)
+        torch.cuda.synchronize()
+        pos = assembly.phase1_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk,
+                                        cfg.topk, sel[0])
+        rot = orope.phase1_rope_positions(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk,
+                                          cfg.topk, sel[0], pos_mode=orope.CONTIGUOUS)
+        qa = _round_bf16(orope.assembled_rope(f64(q[0]), pos, rot, w))
+        ka = _round_bf16(orope.assembled_rope(f64(k[0]), pos, rot, w))
+        o_ref, lse_ref = attention.causal_attention(qa, ka, f64(v[0])[pos], scale)
+        from tests._helpers import check_attention
+        check_attention(o[0].cpu().numpy(), lse[0].cpu().numpy(), o_ref, lse_ref,
+                        f"contiguous block {i}")
+        assert n == len(pos)
+    # Phase-2 tokens start just past the longest assembled input
+    Tq = 3
+    qpos = orope.query_positions(cfg.L, cfg.num_blocks, cfg.sink, cfg.chunk, cfg.topk, Tq,
+                                 G=2, pos_mode=orope.CONTIGUOUS)
+    n_max = P.phase1_len(cfg.L, cfg.num_blocks, cfg.num_blocks - 1, cfg.sink, cfg.chunk,
+                         cfg.topk)
+    xq = workload.bf16_normal(77, (Tq, cfg.Hq, cfg.d))
+    Xq = to_dev_bf16(xq)
+    P.rope_(Xq, None, pos_offset=n_max + 2)
+    torch.cuda.synchronize()
+    ref = orope.rope(f64(xq), qpos, w)
+    check_rounding(_bits(Xq), ref, f64(xq), "contiguous Phase-2 queries")
