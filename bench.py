@@ -173,11 +173,13 @@ def run_main(args):
     O_star = torch.empty((1, n_star, cfg.Hq, cfg.d), dtype=torch.float32, device="cuda")
     ws = torch.empty(P.phase2_workspace_bytes(N, Tq, cfg.Lb, cfg.Hq, cfg.Hkv, cfg.d) or 1,
                      dtype=torch.uint8, device="cuda")
+    idf_ws = torch.empty(max(P.maxidf_workspace_bytes(1, cfg.L, N, cfg.chunk, cfg.vocab), 16),
+                         dtype=torch.uint8, device="cuda")
     t_idf, t_p1, t_p2, t_star = Timer(), Timer(), Timer(), Timer()
 
     def step(timed):
         with (t_idf if timed else _Null()):
-            sel = P.maxidf_summaries(d_ids, N, cfg.chunk, cfg.topk, cfg.vocab)
+            sel = P.maxidf_summaries(d_ids, N, cfg.chunk, cfg.topk, cfg.vocab, workspace=idf_ws)
         with (t_p1 if timed else _Null()):
             # the forward pass yields O for every row and the retained KV(B_15);
             # no LSE is needed downstream of Phase 1
@@ -304,10 +306,12 @@ def run_main(args):
     t_idf8 = Timer()
     ids8 = workload.make_ids(workload.CONFIGS["sweep_128k_b4"], batch=8)
     d_ids8 = torch.from_numpy(ids8).cuda()
-    P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab)
+    ws8 = torch.empty(max(P.maxidf_workspace_bytes(8, cfg.L, N, cfg.chunk, cfg.vocab), 16),
+                      dtype=torch.uint8, device="cuda")
+    P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab, workspace=ws8)
     for _ in range(5):
         with t_idf8:
-            P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab)
+            P.maxidf_summaries(d_ids8, N, cfg.chunk, cfg.topk, cfg.vocab, workspace=ws8)
     torch.cuda.synchronize()
 
     f_star = causal_flops(n_star, cfg.Hq, cfg.d)
@@ -494,11 +498,13 @@ def run_sweep(args):
     for batch in (1, 8, 64, 256, 512, 1024):
         idsb = np.concatenate([ids] * ((batch + B - 1) // B))[:batch]
         d = torch.from_numpy(np.ascontiguousarray(idsb)).cuda()
-        P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab)
+        wsb = torch.empty(max(P.maxidf_workspace_bytes(batch, cfg.L, N, cfg.chunk, cfg.vocab), 16),
+                          dtype=torch.uint8, device="cuda")
+        P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab, workspace=wsb)
         t = Timer()
         for _ in range(5):
             with t:
-                P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab)
+                P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab, workspace=wsb)
         torch.cuda.synchronize()
         ms = t.mean_ms()
         byts = batch * (cfg.L * 4 + N * 32 * 4)

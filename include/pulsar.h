@@ -103,6 +103,12 @@ int pulsar_version(void);
  * idf         out float [batch, vocab], nullable: IDF(t) for every id.
  * A context of no tokens (L == 0, so topk must be 0) has no chunks: nothing
  * is read and only idf, when given, is written (ln(num_blocks) everywhere).
+ * workspace   device buffer of at least pulsar_maxidf_workspace_bytes(...)
+ *             bytes, 16-byte aligned, contents on entry irrelevant; or NULL.
+ *             With it, a small batch runs in three launches split over the
+ *             blocks and the vocabulary; with NULL (or a size query of 0) one
+ *             workgroup takes each sequence.  The results are identical.
+ * EWORKSPACE: a workspace smaller than the size query or misaligned.
  *
  * EINVAL: batch < 0, L < 0, num_blocks < 1, L % num_blocks != 0,
  *         Lb % chunk != 0, chunk < 1, topk < 0 or topk > Lb / chunk,
@@ -115,7 +121,17 @@ int pulsar_version(void);
  */
 int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks,
                             int chunk, int topk, int vocab, int32_t* sel_chunks,
-                            int32_t* chunk_mindf, float* idf, void* stream);
+                            int32_t* chunk_mindf, float* idf, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * Device workspace, in bytes, with which pulsar_maxidf_summaries spreads a
+ * small batch (up to 16 sequences, 2..255 blocks, vocab up to 1310720, at
+ * most 16384 chunks per block) over many compute units: per sequence one
+ * presence bitmap of ceil(vocab / 32) words per block and a df byte table.
+ * 0 when the shapes take the one-workgroup-per-sequence kernels.  Host-only.
+ */
+size_t pulsar_maxidf_workspace_bytes(int batch, int64_t L, int num_blocks, int chunk, int vocab);
 
 /*
  * Chunk summaries under any of the four scorers (Appendix "Scoring Heuristic

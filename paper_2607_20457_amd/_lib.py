@@ -18,7 +18,8 @@ SIGNATURES = {
     "pulsar_status_string": (ctypes.c_char_p, [_c_int]),
     "pulsar_version": (_c_int, []),
     "pulsar_maxidf_summaries": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
-                                         _vp, _vp, _vp, _vp]),
+                                         _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "pulsar_maxidf_workspace_bytes": (_c_size, [_c_int, _c_i64, _c_int, _c_int, _c_int]),
     "pulsar_chunk_summaries": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
                                         _c_int, _vp, _vp, _vp]),
     "pulsar_phase1_len": (_c_i64, [_c_i64, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),

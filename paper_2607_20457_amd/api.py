@@ -44,10 +44,16 @@ def _need(t: torch.Tensor, dtype, name: str):
         raise ValueError(f"{name} must be contiguous")
 
 
+def maxidf_workspace_bytes(batch: int, L: int, num_blocks: int, chunk: int, vocab: int) -> int:
+    return int(_lib.lib().pulsar_maxidf_workspace_bytes(batch, L, num_blocks, chunk, vocab))
+
+
 def maxidf_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, vocab: int,
-                     return_mindf: bool = False, return_idf: bool = False):
+                     return_mindf: bool = False, return_idf: bool = False, workspace="auto"):
     """Top-k Max-IDF chunks per block.  ids int32 [batch, L] ->
-    sel int32 [batch, num_blocks, topk] (+ mindf [batch, N, C], idf [batch, V])."""
+    sel int32 [batch, num_blocks, topk] (+ mindf [batch, N, C], idf [batch, V]).
+    workspace: "auto" allocates the split path's workspace when the shapes
+    use one, None runs one workgroup per sequence, or a device buffer."""
     if ids.dim() == 1:
         ids = ids[None]
     _need(ids, torch.int32, "ids")
@@ -57,8 +63,13 @@ def maxidf_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, 
     sel = torch.empty((batch, num_blocks, topk), dtype=torch.int32, device=dev)
     mindf = torch.empty((batch, num_blocks, C), dtype=torch.int32, device=dev) if return_mindf else None
     idf = torch.empty((batch, vocab), dtype=torch.float32, device=dev) if return_idf else None
+    need = maxidf_workspace_bytes(batch, L, num_blocks, chunk, vocab) if num_blocks > 0 else 0
+    if isinstance(workspace, str):
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need else None
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = _lib.lib().pulsar_maxidf_summaries(_ptr(ids), batch, L, num_blocks, chunk, topk, vocab,
-                                            _ptr(sel), _ptr(mindf), _ptr(idf), _stream())
+                                            _ptr(sel), _ptr(mindf), _ptr(idf), _ptr(workspace),
+                                            ws_bytes, _stream())
     _lib.check(st, "pulsar_maxidf_summaries")
     out = [sel]
     if return_mindf:

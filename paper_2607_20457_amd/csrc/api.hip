@@ -8,7 +8,7 @@
 
 namespace {
 
-constexpr int kVersion = 4;
+constexpr int kVersion = 5;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
@@ -87,9 +87,13 @@ const char* pulsar_status_string(int status) {
 
 int pulsar_version(void) { return kVersion; }
 
+size_t pulsar_maxidf_workspace_bytes(int batch, int64_t L, int num_blocks, int chunk, int vocab) {
+  return maxidf_split_workspace(batch, L, num_blocks, chunk, vocab);
+}
+
 int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
                             int topk, int vocab, int32_t* sel_chunks, int32_t* chunk_mindf,
-                            float* idf, void* stream) {
+                            float* idf, void* workspace, size_t workspace_bytes, void* stream) {
   if (batch < 0 || L < 0 || num_blocks < 1 || vocab < 1 || chunk < 1 || topk < 0)
     return PULSAR_EINVAL;
   if (L % num_blocks != 0) return PULSAR_EINVAL;
@@ -103,6 +107,12 @@ int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_bl
     // no tokens: every df is 0, so IDF(t) = ln(N / 1) and there are no chunks
     if (batch == 0 || idf == nullptr) return PULSAR_OK;
     return launch_idf_fill(idf, (int64_t)batch * vocab, num_blocks, (hipStream_t)stream);
+  }
+  const size_t need = maxidf_split_workspace(batch, L, num_blocks, chunk, vocab);
+  if (need > 0 && workspace != nullptr) {
+    if (workspace_bytes < need || !aligned16(workspace)) return PULSAR_EWORKSPACE;
+    return launch_maxidf_split(ids, batch, L, num_blocks, chunk, topk, vocab, sel_chunks,
+                               chunk_mindf, idf, workspace, (hipStream_t)stream);
   }
   const size_t lds = maxidf_lds_bytes(L, num_blocks, chunk, vocab);
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;

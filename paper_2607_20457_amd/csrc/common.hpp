@@ -151,6 +151,12 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
                   int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf, size_t lds_bytes,
                   hipStream_t stream);
 size_t maxidf_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab);
+// Max-IDF of few sequences split over blocks and vocabulary slices (three
+// launches through a workspace); 0 bytes where that path is not taken.
+size_t maxidf_split_workspace(int batch, int64_t L, int num_blocks, int chunk, int vocab);
+int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                        int topk, int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf,
+                        void* workspace, hipStream_t stream);
 int decode_parts(int n_shards, int64_t S, int Hkv);
 bool decode_applies(int Tq, int Hq, int Hkv, int d);
 // The generation shard of a decode step, folded into the same launch: rows

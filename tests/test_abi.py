@@ -73,7 +73,7 @@ def test_maxidf_validation():
     def call(**kw):
         a = {**ok, **kw}
         return f(a["ids"], a["batch"], a["L"], a["N"], a["m"], a["k"], a["V"], a["sel"], None,
-                 None, None)
+                 None, a.get("ws"), a.get("wsb", 0), None)
     assert call(L=4100) == EINVAL
     assert call(m=24) == EINVAL          # Lb % m
     assert call(k=65) == EINVAL          # k > chunks per block
@@ -88,6 +88,10 @@ def test_maxidf_validation():
     assert call(m=512, L=4 * 1024, k=1) == EUNSUP
     assert call(V=400000) == EUNSUP      # df table beyond one CU's LDS
     assert call(batch=0) == 0            # nothing to do
+    need = _lib.lib().pulsar_maxidf_workspace_bytes(1, 4096, 4, 16, 32000)
+    assert need > 0
+    assert call(ws=FAKE, wsb=need - 1) == EWS
+    assert call(ws=FAKE + 8, wsb=need) == EWS   # misaligned
 
 
 @pytest.mark.parametrize("L,N,V", [(0, 4, 16), (0, 16, 32000), (0, 1, 128256)])
@@ -98,8 +102,8 @@ def test_maxidf_empty_context_launches_nothing(L, N, V):
     # zero rounds, which read 8192 ids per sequence from the NULL pointer.)
     f = _lib.lib().pulsar_maxidf_summaries
     for batch in (1, 3, 300):
-        assert f(None, batch, L, N, 16, 0, V, None, None, None, None) == 0
-    assert f(None, 1, L, N, 16, 1, V, None, None, None, None) == EINVAL  # k > 0 chunks
+        assert f(None, batch, L, N, 16, 0, V, None, None, None, None, 0, None) == 0
+    assert f(None, 1, L, N, 16, 1, V, None, None, None, None, 0, None) == EINVAL  # k > 0
 
 
 def test_attention_validation():
@@ -236,6 +240,20 @@ def test_phase1_gather_validation():
     assert call(base=0.0) == EINVAL                  # rotating needs a base or table
     assert call(d=96) == EUNSUP and call(d=63) == EINVAL
     assert call(batch=0, X=None, out=None) == 0      # nothing to do
+
+
+def test_maxidf_workspace_sizes():
+    ws = _lib.lib().pulsar_maxidf_workspace_bytes
+    # 16 bitmaps of 4008 words and a 128256-byte df table per 128K sequence
+    one = ws(1, 131072, 16, 32, 128256)
+    assert one == ((16 * 4008 * 4 + 31) // 32) * 32 + 4008 * 32
+    assert ws(8, 131072, 16, 32, 128256) == 8 * one
+    assert ws(16, 131072, 16, 32, 128256) == 16 * one
+    assert ws(17, 131072, 16, 32, 128256) == 0     # one workgroup per sequence is as fast
+    assert ws(1, 131072, 1, 32, 128256) == 0       # one block: nothing to split
+    assert ws(1, 131072, 16, 32, 200000) > 0       # bitmaps of vocab / 8 bytes in LDS
+    assert ws(1, 131072, 16, 32, 2000000) == 0     # presence bitmap beyond LDS
+    assert ws(1, 4097, 4, 16, 100) == 0            # invalid shapes take no workspace
 
 
 def test_chunk_summaries_validation():

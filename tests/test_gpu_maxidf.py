@@ -15,21 +15,32 @@ pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
 
 
-def _check(ids, N, m, k, V, idf_too=True):
-    print(f"maxidf parity: batch={ids.shape[0]} L={ids.shape[1]} N={N} m={m} k={k} V={V}",
-          flush=True)
+def _check(ids, N, m, k, V, idf_too=True, single=True):
+    """Both paths against the oracle: with the size query's workspace (split
+    over blocks and vocabulary where the shapes allow) and without one (one
+    workgroup per sequence).  Their outputs must also agree bit for bit."""
     sel_ref, mindf_ref, idf_ref, _ = maxidf.maxidf_summaries(ids, N, m, k, V)
     d_ids = to_dev_i32(ids)
-    if idf_too:
-        sel, mindf, idf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True, return_idf=True)
-    else:
-        sel, mindf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True)
-    torch.cuda.synchronize()
-    assert np.array_equal(mindf.cpu().numpy(), mindf_ref)
-    assert np.array_equal(sel.cpu().numpy(), sel_ref)
-    if idf_too:
-        np.testing.assert_allclose(idf.cpu().numpy(), idf_ref, rtol=2e-6, atol=2e-6)
-    return sel
+    need = P.maxidf_workspace_bytes(ids.shape[0], ids.shape[1], N, m, V)
+    outs = []
+    for ws in (("auto", None) if single else ("auto",)) if need else (None,):
+        print(f"maxidf parity: batch={ids.shape[0]} L={ids.shape[1]} N={N} m={m} k={k} V={V} "
+              f"path={'split' if ws else 'one workgroup per sequence'}", flush=True)
+        if idf_too:
+            sel, mindf, idf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True,
+                                                 return_idf=True, workspace=ws)
+        else:
+            (sel, mindf), idf = P.maxidf_summaries(d_ids, N, m, k, V, return_mindf=True,
+                                                   workspace=ws), None
+        torch.cuda.synchronize()
+        assert np.array_equal(mindf.cpu().numpy(), mindf_ref)
+        assert np.array_equal(sel.cpu().numpy(), sel_ref)
+        if idf_too:
+            np.testing.assert_allclose(idf.cpu().numpy(), idf_ref, rtol=2e-6, atol=2e-6)
+        outs.append((sel, mindf, idf))
+    if len(outs) == 2 and idf_too:
+        assert torch.equal(outs[0][2], outs[1][2])       # the same fp32 IDF values
+    return outs[-1][0]
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b_32k", "llama8b_128k"])
@@ -163,3 +174,26 @@ def test_every_kernel_layout(L, N, m, V, layout):
     ids = workload.zipf_ids(3000 + N + m, L, V)[None]
     print(f"maxidf layout: {layout}", flush=True)
     _check(ids, N, m, min(5, L // N // m), V)
+
+
+@pytest.mark.parametrize("L,N,m,V,batch", [
+    (131072, 16, 32, 128256, 16),   # the largest batch the split path takes
+    (32768, 32, 16, 32000, 12),     # 384 workgroups: more than the chip holds at once
+    (8000, 8, 4, 700, 3),           # blocks of 1000 ids: not a multiple of the workgroup
+    (65536, 4, 256, 5000, 2),       # chunks of 256 ids: minima across wavefronts
+    (40960, 5, 128, 145000, 1),     # a large presence table
+    (4096, 2, 16, 1, 1),            # one id in the vocabulary: every df = N
+])
+def test_split_path_shapes(L, N, m, V, batch):
+    ids = np.stack([workload.zipf_ids(6000 + b + m, L, V) for b in range(min(batch, 4))])
+    ids = ids[np.arange(batch) % ids.shape[0]]
+    assert P.maxidf_workspace_bytes(batch, L, N, m, V) > 0
+    _check(ids, N, m, min(9, L // N // m), V, idf_too=batch <= 4)
+
+
+def test_split_path_large_vocab():
+    # vocabularies the one-workgroup kernels do not take at this length
+    ids = workload.zipf_ids(6100, 40960, 163840)[None]
+    _check(ids, 5, 128, 9, 163840, single=False)
+    ids = workload.zipf_ids(6101, 65536, 1000000)[None]
+    _check(ids, 8, 32, 4, 1000000, single=False)
