@@ -45,7 +45,10 @@ from paper_2607_20457_amd import workload  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak (published)
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E peak (published)
-ATTN_SRC = os.path.join(ROOT, "paper_2607_20457_amd", "csrc", "attn.hip")
+# the attention kernel's sources: the HBM-traffic figure is used only while
+# they are unchanged since the counters were taken
+ATTN_SRCS = [os.path.join(ROOT, "paper_2607_20457_amd", "csrc", f)
+             for f in ("attn_kernel.hpp", "attn.hip", "attn_d128.hip", "common.hpp")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
@@ -61,9 +64,12 @@ def bf16_dev(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
-def src_sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def src_sha(paths):
+    h = hashlib.sha256()
+    for path in paths:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel_key):
@@ -74,7 +80,7 @@ def measured_traffic(kernel_key):
             t = json.load(f)[kernel_key]
     except (OSError, KeyError, ValueError):
         return None
-    if t.get("source_sha") != src_sha(ATTN_SRC):
+    if t.get("source_sha") != src_sha(ATTN_SRCS):
         return None
     return t.get("bytes_per_launch")
 
