@@ -19,8 +19,14 @@
  * - bf16 tensors are passed as raw 16-bit storage (IEEE bfloat16).
  * - Return codes are pulsar_status values; 0 is success.
  * - The library keeps no mutable global state, apart from the static scratch
- *   of pulsar_phase2_query_noalloc (see there); calls on different streams
- *   may run concurrently as long as their output buffers do not overlap.
+ *   of pulsar_phase2_query_noalloc (see there) and the work counters of the
+ *   causal attention launches (pulsar_phase1_attn): a slot of 128 bytes per
+ *   (device, stream) for the first 64 streams of a device, in static device
+ *   memory, zero between launches.  Launches on one stream never overlap;
+ *   launches on other streams use other slots, and a launch captured into a
+ *   graph, or on a stream beyond the slots, uses none (one workgroup per row
+ *   tile).  Calls on different streams may run concurrently as long as their
+ *   output buffers do not overlap.
  */
 #ifndef PULSAR_H_
 #define PULSAR_H_

@@ -6,13 +6,20 @@
 //    split along the keys, giving (o, lse) partials (Algorithm 1, Phase 2).
 //
 // Work decomposition
-//   A workgroup is 8 wavefronts (2 per SIMD), all reading the same
+//   A work item is one row tile of one KV head (and head slice, sequence or
+//   split); a workgroup is 8 wavefronts (2 per SIMD), all reading the same
 //   KV head.  When the group size Hq/Hkv is a multiple of 4, four consecutive
 //   waves are 4 query heads of that group over the same 32*QT rows
 //   (grouped-query sharing: one K/V tile in LDS feeds four heads); further
 //   waves, or smaller groups, split the rows.
-//   Workgroup ids run heaviest causal row tile first, and the KV head is the
-//   fastest-varying index, so with 8 KV heads each XCD's L2 serves one head.
+//   Items run heaviest causal row tile first.  Causal launches are
+//   persistent: one workgroup per CU takes items from a queue per KV head,
+//   its home queue (blockIdx mod Hkv; workgroups are placed on the XCDs
+//   round-robin, so with 8 KV heads each XCD's L2 serves one head) and, once
+//   that is empty, the others' -- the XCDs run at different clocks, and a
+//   fixed share per XCD left the fast ones idle for the last few percent.
+//   Otherwise (Phase 2, or no counter slot) each workgroup is one item,
+//   with the KV head the fastest-varying index of its id.
 //
 // Per wavefront, per 64-key tile, in two 32-key halves (32x32x16 bf16 MFMA,
 // fp32 accumulate)
@@ -56,6 +63,11 @@ struct KernelArgs {
   int rows_per_wg;    // query rows per workgroup
   int n_row_tiles;
   int nz;             // z extent (sequences, or shards x splits)
+  // Persistent causal launch: the work counters of this launch (one per KV
+  // head, then the count of finished workgroups; all zero before the launch
+  // and left zero by it), or null for one workgroup per item.
+  unsigned* sched;
+  int grid;           // workgroups of a persistent launch (one per CU)
 };
 
 // Launch of one instantiation for head dimension D (defined in the per-D
@@ -127,20 +139,57 @@ void attn_fwd_kernel(KernelArgs ka) {
   const AttnLaunch& a = ka.a;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // ---- work items ------------------------------------------------------------
+  // Item k of the queue of KV head h is (head slice, z, row tile) with the
+  // heaviest row tile first; a persistent workgroup holds item h * qlen + k,
+  // one of a plain launch is item k * Hkv + h (its blockIdx).
+  unsigned* const sched = CAUSAL ? ka.sched : nullptr;
+  const bool persistent = sched != nullptr;
+  const int qlen = ka.hsub * ka.nz * ka.n_row_tiles;
+  const int home = blockIdx.x % a.Hkv;
+  __shared__ int s_item;
+  // thread 0: the next item from the home queue, else from the others (a
+  // queue read as exhausted is skipped without an increment); -1 when all
+  // are empty.  Every queue hands out each of its qlen items exactly once.
+  auto claim = [&]() -> int {
+    for (int i = 0; i < a.Hkv; ++i) {
+      const int h = home + i < a.Hkv ? home + i : home + i - a.Hkv;
+      if (__hip_atomic_load(&sched[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >=
+          (unsigned)qlen)
+        continue;
+      const unsigned k = atomicAdd(&sched[h], 1u);
+      if (k < (unsigned)qlen) return h * qlen + (int)k;
+    }
+    return -1;
+  };
+  int item = blockIdx.x;
+  if (persistent) {
+    if (tid == 0) s_item = claim();
+    __syncthreads();
+    item = s_item;
+  }
+  int last_z = -1;
+  while (item >= 0) {
+  int next_item = -1;
+  {  // one item
+  // lane-derived values are re-formed per item from an opaque copy of the
+  // thread index, so that the compiler does not hold them in registers
+  // across items
+  int tid_i = threadIdx.x;
+  asm volatile("" : "+v"(tid_i));
+  const int tid = tid_i;
+  const int lane = tid & 63;
   const int l32 = lane & 31;
   const int g = lane >> 5;
-
-  // ---- workgroup -> (kv head, head slice, z, row tile) ---------------------
-  int bid = blockIdx.x;
-  const int kvh = bid % a.Hkv;
-  bid /= a.Hkv;
-  const int hs = bid % ka.hsub;
-  bid /= ka.hsub;
-  const int z = bid % ka.nz;
-  bid /= ka.nz;
-  const int row_tile = ka.n_row_tiles - 1 - bid;
+  const int kvh = persistent ? item / qlen : item % a.Hkv;
+  int kk = persistent ? item - kvh * qlen : item / a.Hkv;
+  const int hs = kk % ka.hsub;
+  kk /= ka.hsub;
+  const int z = kk % ka.nz;
+  kk /= ka.nz;
+  const int row_tile = ka.n_row_tiles - 1 - kk;
 
   const int head = kvh * ka.group + hs * ka.heads_per_wg + (wave % ka.heads_per_wg);
   const int wg_row0 = row_tile * ka.rows_per_wg;
@@ -166,7 +215,10 @@ void attn_fwd_kernel(KernelArgs ka) {
   int32_t* lpos = reinterpret_cast<int32_t*>(smem + 3 * T::STAGE);  // [3][BN]
   auto pos_of = [&](int t) { return lpos + (t % 3) * BN; };
   int* run_base = lpos + 3 * BN;                                      // [map.n_runs]
-  if constexpr (MODE == MAP_SUMMARY) build_run_table(a.map, sel, run_base, tid, THREADS);
+  __syncthreads();  // the previous item's LDS reads are done
+  if constexpr (MODE == MAP_SUMMARY)
+    if (z != last_z) build_run_table(a.map, sel, run_base, tid, THREADS);
+  last_z = z;
   __syncthreads();
 
   // K/V rows are read through buffer resources covering this sequence (or
@@ -580,6 +632,11 @@ void attn_fwd_kernel(KernelArgs ka) {
   }
   if (__syncthreads_or(overflow)) run_pass(std::true_type{});
 
+  // The next item is claimed only now (its latency overlaps the stores
+  // below): claiming it earlier commits a workgroup to it before it is known
+  // which workgroup frees up first, which spreads the end of the launch.
+  if (persistent && tid == 0) next_item = claim();
+
   // ---- epilogue: normalise, write O and LSE ---------------------------------
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
@@ -611,12 +668,25 @@ void attn_fwd_kernel(KernelArgs ka) {
       }
     }
   }
+  }  // one item
+  if (!persistent) break;
+  __syncthreads();
+  if (threadIdx.x == 0) s_item = next_item;
+  __syncthreads();
+  item = s_item;
+  }  // items
+  // The last workgroup to finish (every claim of every workgroup is done by
+  // then) leaves the counters zero for the next launch on this slot.
+  if (persistent && threadIdx.x == 0 && atomicAdd(&sched[a.Hkv], 1u) == gridDim.x - 1) {
+    for (int h = 0; h <= a.Hkv; ++h) atomicExch(&sched[h], 0u);
+  }
 }
 
 template <int D, int QT, int WAVES, bool CAUSAL, bool LSE, int MODE>
 int launch_impl(const KernelArgs& ka, hipStream_t stream) {
-  const int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
+  int64_t nwg = (int64_t)ka.n_row_tiles * ka.hsub * ka.a.Hkv * ka.nz;
   if (nwg == 0) return PULSAR_OK;
+  if (CAUSAL && ka.sched != nullptr && nwg > ka.grid) nwg = ka.grid;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const int64_t lds = Tile<D>::LDS + (int64_t)ka.a.map.n_runs * 4;
   if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;

@@ -145,6 +145,68 @@ def test_deterministic():
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
 
 
+def _bits_equal(a, b):
+    return a.shape == b.shape and torch.equal(a.contiguous().view(torch.int32),
+                                              b.contiguous().view(torch.int32))
+
+
+def test_causal_launches_on_several_streams():
+    # Causal launches take a work-counter slot per stream and may run at the
+    # same time on different streams: each must equal its result alone,
+    # bit for bit, on every repetition (the counters start from zero again).
+    cfg = workload.CONFIGS["llama8b_32k"]
+    sel, q, k, v = _inputs(cfg)
+    Q, K, V, S = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), to_dev_i32(sel)
+    blocks = [7, 6, 5, 4]
+    run = lambda i: P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S)
+    ref = [run(i) for i in blocks]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in blocks]
+    for rep in range(3):
+        print(f"several streams: repetition {rep}", flush=True)
+        outs = []
+        for i, s in zip(blocks, streams):
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                outs.append(run(i))
+        torch.cuda.synchronize()
+        for (o, lse), (o_r, lse_r), i in zip(outs, ref, blocks):
+            assert _bits_equal(o, o_r) and _bits_equal(lse, lse_r), f"block {i}"
+
+
+def test_causal_launch_in_a_graph_replays():
+    # Captured into a graph the causal launch takes the one-workgroup-per-item
+    # form; every replay, with eager launches between them, must equal the
+    # eager result bit for bit.
+    cfg = workload.CONFIGS["llama8b_32k"]
+    sel, q, k, v = _inputs(cfg)
+    Q, K, V, S = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), to_dev_i32(sel)
+    i = 5
+    n = P.phase1_len(cfg.L, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk)
+    o_eager, lse_eager = P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S)
+    O = torch.empty((1, n, cfg.Hq, cfg.d), dtype=torch.float32, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up outside the capture
+        P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S, out=O)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        _, lse_g = P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S,
+                                 out=O)
+    for rep in range(3):
+        print(f"graph replay {rep}", flush=True)
+        O.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert _bits_equal(O, o_eager) and _bits_equal(lse_g, lse_eager), f"replay {rep}"
+        # eager work between the replays, on the same stream
+        o2, _ = P.phase1_attn(Q, K, V, cfg.num_blocks, i - 1, cfg.sink, cfg.chunk, cfg.topk, S)
+        torch.cuda.synchronize()
+
+
 def test_far_larger_later_score_takes_exact_pass():
     # A key placed after the first 32 keys whose score exceeds the first keys'
     # maximum by far more than 2^64 in weight: the reference-max pass flags
