@@ -79,11 +79,11 @@ int launch_idf_fill(float* idf, int64_t n, int num_blocks, hipStream_t stream) {
 // ---------------------------------------------------------------------------
 // Online-softmax merge (Appendix "Phase 2 Distributed Softmax Merge").
 // Thread = four consecutive head_dim entries of one (z, query, head).  One
-// pass over the parts, eight at a time with all their loads issued
-// together: the running maximum m, s = sum_h exp(l_h - m) and
-// a = sum_h exp(l_h - m) o_h are rescaled when m rises; then l = m + ln s and
-// o = a / s.  -inf partials weigh zero.
-constexpr int kMergeChunk = 8;
+// pass over the parts, CH at a time (2, 4 or 8: the fewest that cover H, up
+// to 8) with all their loads issued together: the running maximum m,
+// s = sum_h exp(l_h - m) and a = sum_h exp(l_h - m) o_h are rescaled when m
+// rises; then l = m + ln s and o = a / s.  -inf partials weigh zero.
+template <int CH>
 __global__ __launch_bounds__(256) void lse_merge_kernel(
     const float* __restrict__ o_parts, const float* __restrict__ lse_parts, int H, int Tq, int Hq,
     int d4, int64_t part_ostride, int64_t part_lstride, float* __restrict__ o,
@@ -102,20 +102,20 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(
   const f32x4* op = reinterpret_cast<const f32x4*>(o_parts) + z * (int64_t)H * (part_ostride / 4);
   float m = -INFINITY, sum = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int p0 = 0; p0 < H; p0 += kMergeChunk) {
-    float l[kMergeChunk];
-    f32x4 v[kMergeChunk];
+  for (int p0 = 0; p0 < H; p0 += CH) {
+    float l[CH];
+    f32x4 v[CH];
 #pragma unroll
-    for (int u = 0; u < kMergeChunk; ++u) {
+    for (int u = 0; u < CH; ++u) {
       const int p = min(p0 + u, H - 1);  // a part past the last re-reads it, weighing zero
       l[u] = lp[p * part_lstride];
       v[u] = op[p * (part_ostride / 4) + orow];
     }
     float cm = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < kMergeChunk; ++u)
+    for (int u = 0; u < CH; ++u)
       if (p0 + u < H) cm = fmaxf(cm, l[u]);
-    // branch-free, so that all sixteen loads are issued before the first
+    // branch-free, so that all 2 CH loads are issued before the first
     // wait; with no finite partial yet the weights are taken against 0 and
     // come out 0
     const float nm = fmaxf(m, cm);
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void lse_merge_kernel(
     sum *= alpha;
     acc *= alpha;
 #pragma unroll
-    for (int u = 0; u < kMergeChunk; ++u) {
+    for (int u = 0; u < CH; ++u) {
       const float w = p0 + u < H ? __expf(l[u] - nm_use) : 0.f;
       sum += w;
       acc += w * v[u];
@@ -204,7 +204,8 @@ int launch_lse_merge(const float* o_parts, const float* lse_parts, int H, int nz
     return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
   }
   const int64_t blocks = (total + 255) / 256;
-  hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, o_parts,
-                     lse_parts, H, Tq, Hq, d / 4, part_ostride, part_lstride, o, lse, total);
+  const auto kern = H <= 2 ? lse_merge_kernel<2> : H <= 4 ? lse_merge_kernel<4> : lse_merge_kernel<8>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, stream, o_parts, lse_parts, H,
+                     Tq, Hq, d / 4, part_ostride, part_lstride, o, lse, total);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }
