@@ -689,7 +689,8 @@ int launch_impl(const KernelArgs& ka, hipStream_t stream) {
   if (CAUSAL && ka.sched != nullptr && nwg > ka.grid) nwg = ka.grid;
   if (nwg > 0x7fffffff) return PULSAR_EUNSUPPORTED;
   const int64_t lds = Tile<D>::LDS + (int64_t)ka.a.map.n_runs * 4;
-  if (lds > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
+  // the kernel's static LDS (the item broadcast) comes on top, aligned
+  if (lds + 16 > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
   auto kern = attn_fwd_kernel<D, QT, WAVES, CAUSAL, LSE, MODE>;
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds) != hipSuccess)
