@@ -174,6 +174,36 @@ def test_causal_launches_on_several_streams():
             assert _bits_equal(o, o_r) and _bits_equal(lse, lse_r), f"block {i}"
 
 
+def test_causal_launches_beyond_the_counter_slots():
+    # 70 streams of their own (more than the 64 counter slots of a device):
+    # the first streams get a slot, the rest the plain launch; every result
+    # equals the one on the default stream, bit for bit.
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime this process already uses
+    hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    cfg = workload.CONFIGS["tiny"]
+    sel, q, k, v = _inputs(cfg)
+    Q, K, V, S = to_dev_bf16(q), to_dev_bf16(k), to_dev_bf16(v), to_dev_i32(sel)
+    i = 3
+    o_ref, lse_ref = P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S)
+    torch.cuda.synchronize()
+    handles = []
+    try:
+        for n in range(70):
+            h = ctypes.c_void_p()
+            assert hip.hipStreamCreate(ctypes.byref(h)) == 0
+            handles.append(h)
+            with torch.cuda.stream(torch.cuda.ExternalStream(h.value)):
+                o, lse = P.phase1_attn(Q, K, V, cfg.num_blocks, i, cfg.sink, cfg.chunk, cfg.topk, S)
+            torch.cuda.synchronize()
+            assert _bits_equal(o, o_ref) and _bits_equal(lse, lse_ref), f"stream {n}"
+    finally:
+        torch.cuda.synchronize()
+        for h in handles:
+            hip.hipStreamDestroy(h)
+
+
 def test_causal_launch_in_a_graph_replays():
     # Captured into a graph the causal launch takes the one-workgroup-per-item
     # form; every replay, with eager launches between them, must equal the
