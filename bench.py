@@ -31,7 +31,9 @@ import hashlib
 import json
 import math
 import os
+import subprocess
 import sys
+import threading
 import time
 
 import numpy as np
@@ -530,6 +532,84 @@ class _Null:
         return False
 
 
+def _smi_sample():
+    """Socket power (W) and per-XCD graphics clocks (MHz) from amd-smi, or None."""
+    try:
+        out = subprocess.run(["amd-smi", "metric", "--power", "--clock"], capture_output=True,
+                             text=True, timeout=10).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    power, clocks, in_gfx = None, [], False
+    for line in out.splitlines():
+        t = line.strip()
+        if t.startswith("SOCKET_POWER:"):
+            try:
+                power = float(t.split()[1])
+            except (IndexError, ValueError):
+                pass
+        elif t.startswith("GFX_"):
+            in_gfx = True
+        elif in_gfx and t.startswith("CLK:"):
+            try:
+                clocks.append(float(t.split()[1]))
+            except (IndexError, ValueError):
+                pass
+            in_gfx = False
+        elif t.endswith(":") and not t.startswith("GFX_"):
+            in_gfx = False
+    return power, clocks
+
+
+def run_power(args):
+    """Phase-1 block 15 (the timed launch) back to back for --power-seconds,
+    with the socket power and the graphics clocks sampled once a second."""
+    cfg = workload.CONFIGS["llama8b_128k"]
+    N, i_last = cfg.num_blocks, cfg.num_blocks - 1
+    ids = workload.make_ids(cfg, batch=1)
+    q, k, v = workload.make_qkv(cfg, batch=1)
+    Q, K, V = bf16_dev(q), bf16_dev(k), bf16_dev(v)
+    sel = P.maxidf_summaries(torch.from_numpy(ids).cuda(), N, cfg.chunk, cfg.topk, cfg.vocab)
+    n = P.phase1_len(cfg.L, N, i_last, cfg.sink, cfg.chunk, cfg.topk)
+    O = torch.empty((1, n, cfg.Hq, cfg.d), dtype=torch.float32, device="cuda")
+    launch = lambda: P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, sel,
+                                   out=O, return_lse=False)
+    for _ in range(3):
+        launch()
+    torch.cuda.synchronize()
+    idle = _smi_sample()
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.wait(1.0):
+            smp = _smi_sample()
+            if smp is not None:
+                samples.append(smp)
+
+    th = threading.Thread(target=sampler)
+    th.start()
+    t0, count = time.time(), 0
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    while time.time() - t0 < args.power_seconds:
+        for _ in range(25):
+            launch()
+        count += 25
+        torch.cuda.synchronize()
+    e1.record()
+    torch.cuda.synchronize()
+    stop.set()
+    th.join()
+    ms = e0.elapsed_time(e1) / count
+    busy = [s for s in samples if s[0] is not None]
+    print(json.dumps({
+        "what": "Phase-1 block 15 (128K workload) back to back; amd-smi samples once a second",
+        "launches": count, "ms_per_launch": ms,
+        "tflops": causal_flops(n, cfg.Hq, cfg.d) / (ms * 1e-3) / 1e12,
+        "idle": None if idle is None else {"socket_power_w": idle[0], "gfx_clk_mhz": idle[1]},
+        "busy": [{"socket_power_w": p, "gfx_clk_mhz": c} for p, c in busy],
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -544,6 +624,9 @@ def main():
                     help="only the warm-up and timed steps (for profiler traces)")
     ap.add_argument("--calibrate", action="store_true",
                     help="append a 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
+    ap.add_argument("--power-seconds", type=float, default=0.0,
+                    help="only Phase-1 block 15 back to back for this long, sampling power "
+                         "and clocks")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the library runs on a single GPU and has "
@@ -552,7 +635,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    if args.sweep:
+    if args.power_seconds > 0:
+        run_power(args)
+    elif args.sweep:
         run_sweep(args)
     else:
         run_main(args)
