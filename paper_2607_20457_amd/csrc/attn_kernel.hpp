@@ -205,10 +205,7 @@ void attn_fwd_kernel(KernelArgs ka) {
 
   const int32_t* sel = a.sel ? a.sel + zkv * a.sel_bstride : nullptr;
   const int64_t q_row = (int64_t)a.Hq * D;
-  const int64_t kv_row = (int64_t)a.Hkv * D;
   const uint16_t* Qz = a.Q + zkv * a.q_zstride + (int64_t)head * D;
-  const uint16_t* Kz = a.K + zkv * a.kv_zstride + (int64_t)kvh * D;
-  const uint16_t* Vz = a.V + zkv * a.kv_zstride + (int64_t)kvh * D;
   const float c2 = a.scale_log2;
 
   lds_u8* const stage0 = (lds_u8*)smem;  // LDS address space: reads take immediate offsets

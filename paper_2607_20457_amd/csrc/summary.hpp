@@ -185,22 +185,29 @@ __device__ __forceinline__ void select_block(const KeyT* cv, int C, uint32_t key
   // valid: the slot holds a chunk of the block; key: its key
 #define SEL_VALID(i) (S > 0 || 64 * (i) + lane < C)
 #define SEL_KEY(i) (S > 0 ? xr[S > 0 ? (i) : 0] : (uint32_t)cv[64 * (i) + lane])
+  // each slot loop is straight-line code with S slots in registers, a plain
+  // loop over the LDS keys otherwise
+  auto for_slots = [&](auto&& f) {
+    if constexpr (S > 0) {
+#pragma unroll
+      for (int i = 0; i < S; ++i) f(i);
+    } else {
+      for (int i = 0; i < n_slots; ++i) f(i);
+    }
+  };
   uint32_t lo = 0, hi = key_hi;  // #(key <= hi) >= k; tau in [lo, hi]
   while (lo < hi) {
     const uint32_t mid = lo + ((hi - lo) >> 1);
     int cnt = 0;
-#pragma unroll 4
-    for (int i = 0; i < n_slots; ++i) cnt += __popcll(__ballot(SEL_VALID(i) && SEL_KEY(i) <= mid));
+    for_slots([&](int i) { cnt += __popcll(__ballot(SEL_VALID(i) && SEL_KEY(i) <= mid)); });
     if (cnt >= topk) hi = mid; else lo = mid + 1;
   }
   const uint32_t tau = lo;
   int n_lt = 0;
-#pragma unroll 4
-  for (int i = 0; i < n_slots; ++i) n_lt += __popcll(__ballot(SEL_VALID(i) && SEL_KEY(i) < tau));
+  for_slots([&](int i) { n_lt += __popcll(__ballot(SEL_VALID(i) && SEL_KEY(i) < tau)); });
   const int need = topk - n_lt;  // kept chunks equal to tau
   int eq_before = 0, out_before = 0;
-#pragma unroll 4
-  for (int i = 0; i < n_slots; ++i) {
+  for_slots([&](int i) {
     const bool valid = SEL_VALID(i);
     const uint32_t x = valid ? SEL_KEY(i) : 0u;
     const uint64_t m_eq = __ballot(valid && x == tau);
@@ -209,7 +216,7 @@ __device__ __forceinline__ void select_block(const KeyT* cv, int C, uint32_t key
     if (keep) dst[out_before + count_below(m_keep)] = 64 * i + lane;
     eq_before += __popcll(m_eq);
     out_before += __popcll(m_keep);
-  }
+  });
 #undef SEL_VALID
 #undef SEL_KEY
 }
