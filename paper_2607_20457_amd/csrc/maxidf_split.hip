@@ -7,21 +7,29 @@
 // the chip idle.  This path splits each sequence over its blocks and its
 // vocabulary, in three launches that communicate through a caller workspace:
 //
-//   presence  one workgroup per (sequence, block j): marks the block's ids in
-//             an LDS bitmap (atomic OR) and copies it to the workspace as P_j
-//             (bit t of word t / 32).  Every word of P_j is written, so
-//             nothing needs clearing beforehand.
+//   presence  one workgroup per (sequence, block j): the block's ids write a
+//             1 into a zeroed LDS table of one byte per id (repeated ids
+//             write the same value, so plain byte stores suffice), which is
+//             packed into the workspace as P_j (bit t of word t / 32).  A
+//             vocabulary whose byte table exceeds LDS sets bits of an LDS
+//             bitmap with atomic OR instead.  Every word of P_j is written,
+//             so nothing needs clearing beforehand.
 //   df        one thread per 32 ids: df(t) = sum_j P_j[t], counted with
 //             bit-sliced adders over the N words (one counter bit per plane),
-//             written as bytes to the workspace df table (and IDF = ln(N /
-//             max(df, 1)) when asked).
-//   select    one workgroup per (sequence, block): looks up the df of each id
-//             of the block, takes each chunk's minimum (lane groups, then an
-//             LDS minimum across wavefronts for chunks wider than 64 ids), and
-//             one wavefront picks the top-k chunks (select_block).
+//             written to the workspace df table: nibbles df - 1 for N <= 16,
+//             else bytes (and IDF = ln(N / max(df, 1)) when asked).
+//   select    one workgroup per (sequence, block): copies the df table into
+//             LDS when it fits there, looks up the df of each id of the
+//             block, takes each chunk's minimum (over the lane's 8 ids, then
+//             its lane group), and one wavefront picks the top-k chunks
+//             (select_block).
+//
+// A thread's id loads carry no bounds branch (a lane past the block re-reads
+// its last ids), so all of them are in flight at once: with a branch around
+// each load the compiler waits for each in turn.
 //
 // Workspace per sequence: N bitmaps of W = ceil(V / 32) words (padded to 32
-// bytes), then the df table of 32 W bytes.
+// bytes), then the df table of 32 W bytes (16 W of them used by nibbles).
 #include "summary.hpp"
 
 namespace {
@@ -63,25 +71,82 @@ __global__ __launch_bounds__(kSplitThreads) void split_presence_kernel(
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       const int x = x0 + u * kSplitThreads + tid;
-      t[u] = x < Lb ? min((uint32_t)seq[x], vmax) : vmax + 1;
+      // a lane past the block re-reads the block's last id: marking it again
+      // changes nothing, and such lanes form no chunk (Lb is a multiple of
+      // the chunk); without a branch all kU loads are issued together
+      t[u] = min((uint32_t)seq[min(x, Lb - 1)], vmax);
     }
 #pragma unroll
     for (int u = 0; u < kU; ++u)
-      if (t[u] <= vmax) atomicOr(&bm[t[u] >> 5], 1u << (t[u] & 31));
+      atomicOr(&bm[t[u] >> 5], 1u << (t[u] & 31));
   }
   __syncthreads();
   uint32_t* bits = reinterpret_cast<uint32_t*>(ws + b * seq_bytes) + (int64_t)j * W;
   for (int w = tid; w < W; w += kSplitThreads) bits[w] = bm[w];
 }
 
+// Block j of sequence b with a byte per id: the block's ids write 1 into a
+// zeroed LDS byte table (repeated ids write the same value, so plain byte
+// stores suffice), then each 32 bytes are packed into the word of P_j.
+// Needs 32 W bytes of LDS.
+__global__ __launch_bounds__(kSplitThreads) void split_presence_bytes_kernel(
+    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int vocab,
+    uint8_t* __restrict__ ws, int64_t seq_bytes) {
+  extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+  uint8_t* const pb = reinterpret_cast<uint8_t*>(lds);
+  uint4* const p16 = reinterpret_cast<uint4*>(lds);
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x / num_blocks;
+  const int j = blockIdx.x - (int)(b * num_blocks);
+  const int W = (int)split_words(vocab);
+  const uint32_t vmax = (uint32_t)(vocab - 1);
+  const int32_t* seq = ids + b * L + (int64_t)j * Lb;
+  auto load = [&](int x0, uint32_t (&t)[kU]) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int x = x0 + u * kSplitThreads + tid;
+      // a lane past the block re-reads the block's last id: marking it again
+      // changes nothing, and such lanes form no chunk (Lb is a multiple of
+      // the chunk); without a branch all kU loads are issued together
+      t[u] = min((uint32_t)seq[min(x, Lb - 1)], vmax);
+    }
+  };
+  // the first ids are in flight while the table is cleared
+  uint32_t t[kU];
+  load(0, t);
+  for (int w = tid; w < 2 * W; w += kSplitThreads) p16[w] = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  for (int x0 = 0; x0 < Lb; x0 += kU * kSplitThreads) {
+    if (x0 > 0) load(x0, t);
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      pb[t[u]] = 1;
+  }
+  __syncthreads();
+  // byte k of a 4-byte group (0 or 1) lands on bit 24 + k of x * 0x01020408
+  // (the other partial products fall on distinct bits below 24)
+  uint32_t* bits = reinterpret_cast<uint32_t*>(ws + b * seq_bytes) + (int64_t)j * W;
+  for (int w = tid; w < W; w += kSplitThreads) {
+    const uint4 lo = p16[2 * w], hi = p16[2 * w + 1];
+    const uint32_t g[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    uint32_t v = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v |= ((g[i] * 0x01020408u) >> 24) << (4 * i);
+    bits[w] = v;
+  }
+}
+
 // df of ids 32g .. 32g+31 of sequence b from the N presence words: bit-sliced
-// counters (plane p holds bit p of the 32 counts), then each count becomes a
-// byte of the df table.
-template <int P>
+// counters (plane p holds bit p of the 32 counts), then each count becomes an
+// entry of the df table: a byte, or with NIB (N <= 16) the nibble df - 1.
+// Every id that is looked up occurs in its own block, so its df is 1 .. N and
+// df - 1 fits in 4 bits; the nibble of an absent id is never read.
+template <int P, bool NIB>
 __global__ __launch_bounds__(kDfThreads) void split_df_kernel(int num_blocks, int vocab,
                                                               int slices, uint8_t* __restrict__ ws,
                                                               int64_t seq_bytes,
                                                               float* __restrict__ idf) {
+  constexpr int KD = P <= 5 ? 16 : kU;  // words loaded together
   const int64_t b = blockIdx.x / slices;
   const int g = (blockIdx.x - (int)(b * slices)) * kDfThreads + threadIdx.x;
   const int W = (int)split_words(vocab);
@@ -91,13 +156,12 @@ __global__ __launch_bounds__(kDfThreads) void split_df_kernel(int num_blocks, in
   uint32_t c[P];
 #pragma unroll
   for (int p = 0; p < P; ++p) c[p] = 0u;
-  // kU blocks' words are loaded together before they are added
-  for (int j0 = 0; j0 < num_blocks; j0 += kU) {
-    uint32_t w[kU];
+  for (int j0 = 0; j0 < num_blocks; j0 += KD) {
+    uint32_t w[KD];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) w[u] = j0 + u < num_blocks ? bits[(int64_t)(j0 + u) * W + g] : 0u;
+    for (int u = 0; u < KD; ++u) w[u] = j0 + u < num_blocks ? bits[(int64_t)(j0 + u) * W + g] : 0u;
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
+    for (int u = 0; u < KD; ++u) {
       uint32_t carry = w[u];
 #pragma unroll
       for (int p = 0; p < P; ++p) {
@@ -107,75 +171,143 @@ __global__ __launch_bounds__(kDfThreads) void split_df_kernel(int num_blocks, in
       }
     }
   }
-  // bytes 4r .. 4r+3 of the 32 counts: bit p of count 4r+q is bit 4r+q of
-  // plane p; (nibble * 0x00204081) & 0x01010101 spreads a nibble's bits to
-  // the low bits of four bytes
-  u32x4 out[2];
+  uint8_t* const table = seq_ws + split_bits_bytes(num_blocks, vocab);
+  if constexpr (NIB) {
+    // planes of count - 1 (a borrow chain), then nibble k of the 16 bytes =
+    // bit k of the four planes; spread() moves bit i of a byte to bit 4 i
+    uint32_t e[4];
+    uint32_t borrow = 0xFFFFFFFFu;
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    uint32_t v = 0;
+    for (int p = 0; p < 4; ++p) {
+      e[p] = c[p] ^ borrow;
+      borrow &= ~c[p];
+    }
+    auto spread = [](uint32_t x) {
+      x = (x | (x << 12)) & 0x000F000Fu;
+      x = (x | (x << 6)) & 0x03030303u;
+      return (x | (x << 3)) & 0x11111111u;
+    };
+    u32x4 out;
 #pragma unroll
-    for (int p = 0; p < P; ++p) v |= (((c[p] >> (4 * r)) & 0xFu) * 0x00204081u & 0x01010101u) << p;
-    out[r >> 2][r & 3] = v;
+    for (int r = 0; r < 4; ++r) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) v |= spread((e[p] >> (8 * r)) & 0xFFu) << p;
+      out[r] = v;
+    }
+    reinterpret_cast<u32x4*>(table)[g] = out;
+  } else {
+    // bytes 4r .. 4r+3 of the 32 counts: bit p of count 4r+q is bit 4r+q of
+    // plane p; (nibble * 0x00204081) & 0x01010101 spreads a nibble's bits to
+    // the low bits of four bytes
+    u32x4 out[2];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int p = 0; p < P; ++p) v |= (((c[p] >> (4 * r)) & 0xFu) * 0x00204081u & 0x01010101u) << p;
+      out[r >> 2][r & 3] = v;
+    }
+    u32x4* df = reinterpret_cast<u32x4*>(table) + 2 * (int64_t)g;
+    df[0] = out[0];
+    df[1] = out[1];
   }
-  u32x4* df = reinterpret_cast<u32x4*>(seq_ws + split_bits_bytes(num_blocks, vocab)) + 2 * (int64_t)g;
-  df[0] = out[0];
-  df[1] = out[1];
   if (idf) {
     const float n = (float)num_blocks;
     float* dst = idf + b * vocab;
 #pragma unroll
     for (int k = 0; k < 32; ++k) {
       const int t = 32 * g + k;
-      const uint32_t d = (out[k >> 4][(k >> 2) & 3] >> (8 * (k & 3))) & 0xFFu;
+      uint32_t d = 0;
+#pragma unroll
+      for (int p = 0; p < P; ++p) d |= ((c[p] >> k) & 1u) << p;
       if (t < vocab) dst[t] = logf(n / (float)(d > 1u ? d : 1u));
     }
   }
 }
 
 // Block j of sequence b: the df of each id, each chunk's minimum, the top-k
-// chunks.  Chunk c of the block is ids c*m .. c*m+m-1; lane groups of
-// min(m, 64) lanes take their minimum, and chunks wider than a wavefront
-// combine their groups with an LDS atomic minimum.
+// chunks.  In round r thread tid holds the 8 consecutive ids
+// 8 (1024 r + tid) .. +7 of the block (two 16-byte groups), so a chunk of m
+// ids is one group (m = 4) or m / 8 adjacent lanes: the lane takes the
+// minimum of its ids, then its lane group (at most 32 lanes, within one
+// wavefront).  With DF_LDS the df table (32 W bytes) is first copied into
+// LDS with 16-byte loads, issued together with the ids' loads, and the
+// look-ups read LDS; otherwise they gather from the workspace.
+template <bool DF_LDS, bool NIB>
 __global__ __launch_bounds__(kSplitThreads) void split_select_kernel(
     const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2, int topk,
     int vocab, const uint8_t* __restrict__ ws, int64_t seq_bytes, int32_t* __restrict__ sel,
     int32_t* __restrict__ chunk_mindf) {
-  extern __shared__ __attribute__((aligned(16))) uint32_t cmin[];  // [C]
+  extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int64_t b = blockIdx.x / num_blocks;
   const int j = blockIdx.x - (int)(b * num_blocks);
   const int C = Lb >> chunk_log2;
+  const int W = (int)split_words(vocab);
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const uint8_t* df = ws + b * seq_bytes + split_bits_bytes(num_blocks, vocab);
-  const int32_t* seq = ids + b * L + (int64_t)j * Lb;
-  const int group = min(1 << chunk_log2, 64);
-  const bool wide = chunk_log2 > 6;
-  if (wide)
-    for (int c = tid; c < C; c += kSplitThreads) cmin[c] = 0xFFFFFFFFu;
-  __syncthreads();
-  // kU ids per thread at a time: their loads, then their df lookups, are
-  // issued together.  Every lane of a wavefront runs the same trip count, so
-  // all join the cross-lane minimum; ids past the block read as df 255.
-  for (int x0 = 0; x0 < Lb; x0 += kU * kSplitThreads) {
-    uint32_t t[kU], d[kU];
+  const uint8_t* const dfl = reinterpret_cast<const uint8_t*>(lds);
+  const int tab16 = NIB ? W : 2 * W;  // 16-byte units of the df table
+  uint32_t* const cmin = DF_LDS ? lds + 4 * tab16 : lds;  // [C]
+  const int4* seq4 = reinterpret_cast<const int4*>(ids + b * L + (int64_t)j * Lb);
+  const int ngroups = Lb >> 2;  // 16-byte groups of the block (Lb is a multiple of 4)
+  // Groups past the block re-read its last group: their lanes record no chunk
+  // (Lb is a multiple of the chunk, so no chunk or lane group straddles it),
+  // and without a branch every load is issued at once.
+  auto load = [&](int r, int4 (&q)[2]) {
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int x = x0 + u * kSplitThreads + tid;
-      t[u] = x < Lb ? min((uint32_t)seq[x], vmax) : vmax + 1;
-    }
+    for (int h = 0; h < 2; ++h) q[h] = seq4[min(2 * (r * kSplitThreads + tid) + h, ngroups - 1)];
+  };
+  int4 q[2];
+  load(0, q);
+  if constexpr (DF_LDS) {
+    // every lane stores: lanes past the table copy its last 16 bytes onto
+    // themselves, so neither the loads nor the stores need a branch
+    constexpr int kCopy = PULSAR_LDS_BYTES / 16 / kSplitThreads;
+    const uint4* src = reinterpret_cast<const uint4*>(df);
+    uint4* dst = reinterpret_cast<uint4*>(lds);
+    uint4 r[kCopy];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) d[u] = t[u] <= vmax ? (uint32_t)df[t[u]] : 0xFFu;
+    for (int k = 0; k < kCopy; ++k) r[k] = src[min(k * kSplitThreads + tid, tab16 - 1)];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int x = x0 + u * kSplitThreads + tid;
-      const uint32_t m = group_min(d[u], group);
-      if (x < Lb && (x & (group - 1)) == 0) {
-        const int c = x >> chunk_log2;
-        if (wide) atomicMin(&cmin[c], m);
-        else cmin[c] = m;
+    for (int k = 0; k < kCopy; ++k) dst[min(k * kSplitThreads + tid, tab16 - 1)] = r[k];
+    // the first ids arrive before the barrier, not after it
+    asm volatile("" : "+v"(q[0].x), "+v"(q[0].y), "+v"(q[0].z), "+v"(q[0].w), "+v"(q[1].x),
+                 "+v"(q[1].y), "+v"(q[1].z), "+v"(q[1].w));
+    __syncthreads();
+  }
+  const int nrounds = (ngroups + 2 * kSplitThreads - 1) / (2 * kSplitThreads);
+  for (int rd = 0; rd < nrounds; ++rd) {
+    if (rd > 0) load(rd, q);
+    const uint32_t t[8] = {(uint32_t)q[0].x, (uint32_t)q[0].y, (uint32_t)q[0].z, (uint32_t)q[0].w,
+                           (uint32_t)q[1].x, (uint32_t)q[1].y, (uint32_t)q[1].z, (uint32_t)q[1].w};
+    uint32_t d[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t ti = min(t[i], vmax);
+      if (NIB) {
+        const uint32_t x = DF_LDS ? dfl[ti >> 1] : df[ti >> 1];
+        d[i] = ((x >> ((ti & 1u) << 2)) & 0xFu) + 1u;
+      } else {
+        d[i] = DF_LDS ? dfl[ti] : df[ti];
       }
+    }
+    const int g0 = 2 * (rd * kSplitThreads + tid);  // the lane's first group
+    if (chunk_log2 == 2) {
+      // chunks of 4 ids: each group is a chunk of its own
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        if (g0 + h < ngroups)
+          cmin[g0 + h] = min(min(d[4 * h], d[4 * h + 1]), min(d[4 * h + 2], d[4 * h + 3]));
+    } else {
+      uint32_t m = d[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) m = min(m, d[i]);
+      const int lg = chunk_log2 - 3;  // log2 of the lanes per chunk
+      m = group_min(m, 1 << lg);
+      if (g0 < ngroups && (tid & ((1 << lg) - 1)) == 0) cmin[g0 >> (lg + 1)] = m;
     }
   }
   __syncthreads();
@@ -214,32 +346,50 @@ int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks
   const int64_t seq_bytes = split_seq_bytes(num_blocks, vocab);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   const int64_t grid = (int64_t)batch * num_blocks;
-  const size_t tab = (size_t)split_words(vocab) * 4;
-  if (hipFuncSetAttribute((const void*)split_presence_kernel,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)tab) != hipSuccess)
-    return PULSAR_EHIP;
-  hipLaunchKernelGGL(split_presence_kernel, dim3((unsigned)grid), dim3(kSplitThreads), tab, stream,
-                     ids, L, num_blocks, Lb, vocab, ws, seq_bytes);
+  const size_t bytes_tab = (size_t)split_words(vocab) * 32;
+  if (bytes_tab <= PULSAR_LDS_BYTES) {
+    if (hipFuncSetAttribute((const void*)split_presence_bytes_kernel,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes_tab) != hipSuccess)
+      return PULSAR_EHIP;
+    hipLaunchKernelGGL(split_presence_bytes_kernel, dim3((unsigned)grid), dim3(kSplitThreads),
+                       bytes_tab, stream, ids, L, num_blocks, Lb, vocab, ws, seq_bytes);
+  } else {
+    const size_t tab = (size_t)split_words(vocab) * 4;
+    if (hipFuncSetAttribute((const void*)split_presence_kernel,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)tab) != hipSuccess)
+      return PULSAR_EHIP;
+    hipLaunchKernelGGL(split_presence_kernel, dim3((unsigned)grid), dim3(kSplitThreads), tab,
+                       stream, ids, L, num_blocks, Lb, vocab, ws, seq_bytes);
+  }
   if (hipGetLastError() != hipSuccess) return PULSAR_EHIP;
   const int slices = (int)((split_words(vocab) + kDfThreads - 1) / kDfThreads);
   const dim3 dgrid((unsigned)(batch * slices));
-  // counter planes: enough bits for num_blocks (<= 255)
+  // counter planes: enough bits for num_blocks (<= 255); a nibble table for
+  // up to 16 blocks
+  const bool nib = num_blocks <= 16;
   if (num_blocks < 16)
-    hipLaunchKernelGGL(split_df_kernel<4>, dgrid, dim3(kDfThreads), 0, stream, num_blocks, vocab,
-                       slices, ws, seq_bytes, idf);
+    hipLaunchKernelGGL((split_df_kernel<4, true>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
+                       vocab, slices, ws, seq_bytes, idf);
+  else if (num_blocks == 16)
+    hipLaunchKernelGGL((split_df_kernel<5, true>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
+                       vocab, slices, ws, seq_bytes, idf);
   else if (num_blocks < 32)
-    hipLaunchKernelGGL(split_df_kernel<5>, dgrid, dim3(kDfThreads), 0, stream, num_blocks, vocab,
-                       slices, ws, seq_bytes, idf);
+    hipLaunchKernelGGL((split_df_kernel<5, false>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
+                       vocab, slices, ws, seq_bytes, idf);
   else
-    hipLaunchKernelGGL(split_df_kernel<8>, dgrid, dim3(kDfThreads), 0, stream, num_blocks, vocab,
-                       slices, ws, seq_bytes, idf);
+    hipLaunchKernelGGL((split_df_kernel<8, false>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
+                       vocab, slices, ws, seq_bytes, idf);
   if (hipGetLastError() != hipSuccess) return PULSAR_EHIP;
   const size_t cl = (size_t)(Lb >> chunk_log2) * 4;
-  if (hipFuncSetAttribute((const void*)split_select_kernel,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)cl) != hipSuccess)
+  const size_t df_tab = (size_t)split_words(vocab) * (nib ? 16 : 32);
+  const bool df_lds = df_tab + cl <= PULSAR_LDS_BYTES;
+  auto sk = df_lds ? (nib ? split_select_kernel<true, true> : split_select_kernel<true, false>)
+                   : (nib ? split_select_kernel<false, true> : split_select_kernel<false, false>);
+  const size_t sl = df_lds ? df_tab + cl : cl;
+  if (hipFuncSetAttribute((const void*)sk, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sl) !=
+      hipSuccess)
     return PULSAR_EHIP;
-  hipLaunchKernelGGL(split_select_kernel, dim3((unsigned)grid), dim3(kSplitThreads), cl, stream,
-                     ids, L, num_blocks, Lb, chunk_log2, topk, vocab, ws, seq_bytes, sel,
-                     chunk_mindf);
+  hipLaunchKernelGGL(sk, dim3((unsigned)grid), dim3(kSplitThreads), sl, stream, ids, L, num_blocks,
+                     Lb, chunk_log2, topk, vocab, ws, seq_bytes, sel, chunk_mindf);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }

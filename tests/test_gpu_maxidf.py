@@ -183,6 +183,7 @@ def test_every_kernel_layout(L, N, m, V, layout):
     (65536, 4, 256, 5000, 2),       # chunks of 256 ids: minima across wavefronts
     (40960, 5, 128, 145000, 1),     # a large presence table
     (4096, 2, 16, 1, 1),            # one id in the vocabulary: every df = N
+    (24576, 24, 16, 32000, 3),      # 24 blocks: df bytes (more than 16 blocks), held in LDS
 ])
 def test_split_path_shapes(L, N, m, V, batch):
     ids = np.stack([workload.zipf_ids(6000 + b + m, L, V) for b in range(min(batch, 4))])
@@ -197,3 +198,6 @@ def test_split_path_large_vocab():
     _check(ids, 5, 128, 9, 163840, single=False)
     ids = workload.zipf_ids(6101, 65536, 1000000)[None]
     _check(ids, 8, 32, 4, 1000000, single=False)
+    # 24 blocks and a df byte table too large for LDS: looked up in the workspace
+    ids = np.stack([workload.zipf_ids(6102 + b, 49152, 300000) for b in range(2)])
+    _check(ids, 24, 32, 5, 300000, single=False)
