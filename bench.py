@@ -87,15 +87,26 @@ def measured_traffic(kernel_key):
     return t.get("bytes_per_launch")
 
 
-class Timer:
-    """HIP events on the current stream around each launch of one kernel."""
+# GPU clock cycles of the spin kernel that precedes a short timed call
+SPIN_CYCLES = 400_000
 
-    def __init__(self):
+
+class Timer:
+    """HIP events on the current stream around each launch of one kernel.
+    spin=True first queues a short spin kernel, so that the host has queued
+    the timed call before its start event runs: the events then bracket the
+    device's time alone, not the host's launch overhead (which otherwise
+    dominates calls of a few microseconds)."""
+
+    def __init__(self, spin: bool = False):
         self.pairs = []
+        self.spin = spin
 
     def __enter__(self):
         self.s = torch.cuda.Event(enable_timing=True)
         self.e = torch.cuda.Event(enable_timing=True)
+        if self.spin:
+            torch.cuda._sleep(SPIN_CYCLES)
         self.s.record()
         return self
 
@@ -183,7 +194,7 @@ def run_main(args):
                      dtype=torch.uint8, device="cuda")
     idf_ws = torch.empty(max(P.maxidf_workspace_bytes(1, cfg.L, N, cfg.chunk, cfg.vocab), 16),
                          dtype=torch.uint8, device="cuda")
-    t_idf, t_p1, t_p2, t_star = Timer(), Timer(), Timer(), Timer()
+    t_idf, t_p1, t_p2, t_star = Timer(), Timer(), Timer(), Timer(spin=True)
 
     def step(timed):
         with (t_idf if timed else _Null()):
@@ -237,7 +248,7 @@ def run_main(args):
 
     # Max-IDF throughput: 1024 sequences of 128K ids (512 MiB of ids), every
     # compute unit busy; the batch-1 call in the step is latency-bound on one
-    t_idf_big = Timer()
+    t_idf_big = Timer(spin=True)
     big = d_ids.expand(IDF_THROUGHPUT_BATCH, cfg.L).contiguous()
     P.maxidf_summaries(big, N, cfg.chunk, cfg.topk, cfg.vocab)
     for _ in range(5):
@@ -254,7 +265,7 @@ def run_main(args):
                      ("entropy", P.SCORE_ENTROPY)):
         row = {}
         for batch, inp in ((1, d_ids), (256, big)):
-            t = Timer()
+            t = Timer(spin=True)
             P.chunk_summaries(inp, N, cfg.chunk, cfg.topk, cfg.vocab, sc)
             for _ in range(5):
                 with t:
@@ -266,7 +277,7 @@ def run_main(args):
     del big
 
     # Phase 1 of block 15 with the Even-Spaced baseline prefix (same row count)
-    t_even = Timer()
+    t_even = Timer(spin=True)
     for _ in range(2):
         P.phase1_attn(Q, K, V, N, i_last, cfg.sink, cfg.chunk, cfg.topk, None, P.PREFIX_EVEN,
                       out=O, return_lse=False)
@@ -279,7 +290,7 @@ def run_main(args):
     # Rotary embedding of the layer's Q and K at their global positions (the
     # sparse-position mode), once per layer for the whole context; on copies,
     # so that the attention inputs above stay as drawn
-    t_rope = Timer()
+    t_rope = Timer(spin=True)
     Qr, Kr = Q.clone(), K.clone()
     P.rope_(Qr)
     P.rope_(Kr)
@@ -298,7 +309,7 @@ def run_main(args):
     shards_k = K[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
     shards_v = V[0].view(N, cfg.Lb, cfg.Hkv, cfg.d)
     q_dec = q_dev[:1].contiguous()
-    t_enc, t_dec = Timer(), Timer()
+    t_enc, t_dec = Timer(spin=True), Timer(spin=True)
     for _ in range(2):
         P.phase2_query(q_dev, kg[:Tq], vg[:Tq], 0, shards_k, shards_v)
         P.phase2_query(q_dec, kg, vg, Tq, shards_k, shards_v)
@@ -311,7 +322,7 @@ def run_main(args):
     kv_bytes = 2 * N * cfg.Lb * cfg.Hkv * cfg.d * 2
 
     # Max-IDF at batch 8 (the sweep's setting): latency-bound, 8 compute units
-    t_idf8 = Timer()
+    t_idf8 = Timer(spin=True)
     ids8 = workload.make_ids(workload.CONFIGS["sweep_128k_b4"], batch=8)
     d_ids8 = torch.from_numpy(ids8).cuda()
     ws8 = torch.empty(max(P.maxidf_workspace_bytes(8, cfg.L, N, cfg.chunk, cfg.vocab), 16),
@@ -446,7 +457,7 @@ def cfg5_sweep(reps=3):
         O = torch.empty((B, n_s, cfg.Hq, cfg.d), dtype=torch.bfloat16, device="cuda")
         P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, 0, None, P.PREFIX_ANCHOR,
                       o_dtype=P.OUT_BF16, return_lse=False, out=O)
-        t = Timer()
+        t = Timer(spin=True)
         for _ in range(reps):
             with t:
                 P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, 0, None, P.PREFIX_ANCHOR,
@@ -464,7 +475,7 @@ def cfg5_sweep(reps=3):
             O = torch.empty((B, n_i, cfg.Hq, cfg.d), dtype=torch.bfloat16, device="cuda")
             P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, topk, sel, o_dtype=P.OUT_BF16,
                           return_lse=False, out=O)
-            t = Timer()
+            t = Timer(spin=True)
             for _ in range(reps):
                 with t:
                     P.phase1_attn(Q, K, V, N, i, cfg.sink, cfg.chunk, topk, sel,
@@ -509,7 +520,7 @@ def run_sweep(args):
         wsb = torch.empty(max(P.maxidf_workspace_bytes(batch, cfg.L, N, cfg.chunk, cfg.vocab), 16),
                           dtype=torch.uint8, device="cuda")
         P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab, workspace=wsb)
-        t = Timer()
+        t = Timer(spin=True)
         for _ in range(5):
             with t:
                 P.maxidf_summaries(d, N, cfg.chunk, 32, cfg.vocab, workspace=wsb)
