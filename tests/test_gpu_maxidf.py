@@ -184,6 +184,7 @@ def test_every_kernel_layout(L, N, m, V, layout):
     (40960, 5, 128, 145000, 1),     # a large presence table
     (4096, 2, 16, 1, 1),            # one id in the vocabulary: every df = N
     (24576, 24, 16, 32000, 3),      # 24 blocks: df bytes (more than 16 blocks), held in LDS
+    (26000, 2, 8, 5000, 2),         # blocks of 13000 ids: two rounds of loads, the second partial
 ])
 def test_split_path_shapes(L, N, m, V, batch):
     ids = np.stack([workload.zipf_ids(6000 + b + m, L, V) for b in range(min(batch, 4))])
