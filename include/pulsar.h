@@ -134,8 +134,10 @@ int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_bl
  * Device workspace, in bytes, with which pulsar_maxidf_summaries spreads a
  * small batch (up to 16 sequences, 2..255 blocks, vocab up to 1310720, at
  * most 16384 chunks per block) over many compute units: per sequence one
- * presence bitmap of ceil(vocab / 32) words per block and a df byte table.
- * 0 when the shapes take the one-workgroup-per-sequence kernels.  Host-only.
+ * presence bitmap of ceil(vocab / 32) words per block and a df table of
+ * 32 ceil(vocab / 32) bytes (a byte per id, or a nibble per id when
+ * num_blocks <= 16).  0 when the shapes take the one-workgroup-per-sequence
+ * kernels.  Host-only.
  */
 size_t pulsar_maxidf_workspace_bytes(int batch, int64_t L, int num_blocks, int chunk, int vocab);
 
