@@ -226,14 +226,29 @@ __global__ __launch_bounds__(kDfThreads) void split_df_kernel(int num_blocks, in
   }
 }
 
+// Copy of n 16-byte units (K rounds of kSplitThreads, n > (K - 1) *
+// kSplitThreads) from global memory into LDS: all K loads are issued before
+// the first store.  Lanes past the end copy the last unit onto itself, so no
+// lane branches on its own load or store.
+template <int K>
+__device__ __forceinline__ void copy_rounds(const uint4* __restrict__ src, uint4* dst, int n,
+                                            int tid) {
+  uint4 r[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) r[k] = src[min(k * kSplitThreads + tid, n - 1)];
+#pragma unroll
+  for (int k = 0; k < K; ++k) dst[min(k * kSplitThreads + tid, n - 1)] = r[k];
+}
+
 // Block j of sequence b: the df of each id, each chunk's minimum, the top-k
 // chunks.  In round r thread tid holds the 8 consecutive ids
 // 8 (1024 r + tid) .. +7 of the block (two 16-byte groups), so a chunk of m
 // ids is one group (m = 4) or m / 8 adjacent lanes: the lane takes the
 // minimum of its ids, then its lane group (at most 32 lanes, within one
-// wavefront).  With DF_LDS the df table (32 W bytes) is first copied into
-// LDS with 16-byte loads, issued together with the ids' loads, and the
-// look-ups read LDS; otherwise they gather from the workspace.
+// wavefront).  With DF_LDS the df table (32 W bytes, or 16 W of nibbles) is
+// first copied into LDS with 16-byte loads, issued together with the ids'
+// loads, and the look-ups read LDS; otherwise they gather from the
+// workspace.
 template <bool DF_LDS, bool NIB>
 __global__ __launch_bounds__(kSplitThreads) void split_select_kernel(
     const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int chunk_log2, int topk,
@@ -263,16 +278,23 @@ __global__ __launch_bounds__(kSplitThreads) void split_select_kernel(
   int4 q[2];
   load(0, q);
   if constexpr (DF_LDS) {
-    // every lane stores: lanes past the table copy its last 16 bytes onto
-    // themselves, so neither the loads nor the stores need a branch
-    constexpr int kCopy = PULSAR_LDS_BYTES / 16 / kSplitThreads;
+    // as many rounds of 16-byte units as the table needs (it fits in LDS,
+    // so at most PULSAR_LDS_BYTES / 16 / kSplitThreads = 10)
+    static_assert(PULSAR_LDS_BYTES / 16 / kSplitThreads == 10, "copy rounds below");
     const uint4* src = reinterpret_cast<const uint4*>(df);
     uint4* dst = reinterpret_cast<uint4*>(lds);
-    uint4 r[kCopy];
-#pragma unroll
-    for (int k = 0; k < kCopy; ++k) r[k] = src[min(k * kSplitThreads + tid, tab16 - 1)];
-#pragma unroll
-    for (int k = 0; k < kCopy; ++k) dst[min(k * kSplitThreads + tid, tab16 - 1)] = r[k];
+    switch ((tab16 + kSplitThreads - 1) / kSplitThreads) {
+      case 1: copy_rounds<1>(src, dst, tab16, tid); break;
+      case 2: copy_rounds<2>(src, dst, tab16, tid); break;
+      case 3: copy_rounds<3>(src, dst, tab16, tid); break;
+      case 4: copy_rounds<4>(src, dst, tab16, tid); break;
+      case 5: copy_rounds<5>(src, dst, tab16, tid); break;
+      case 6: copy_rounds<6>(src, dst, tab16, tid); break;
+      case 7: copy_rounds<7>(src, dst, tab16, tid); break;
+      case 8: copy_rounds<8>(src, dst, tab16, tid); break;
+      case 9: copy_rounds<9>(src, dst, tab16, tid); break;
+      default: copy_rounds<10>(src, dst, tab16, tid); break;
+    }
     // the first ids arrive before the barrier, not after it
     asm volatile("" : "+v"(q[0].x), "+v"(q[0].y), "+v"(q[0].z), "+v"(q[0].w), "+v"(q[1].x),
                  "+v"(q[1].y), "+v"(q[1].z), "+v"(q[1].w));
