@@ -26,7 +26,10 @@
  *   launches on other streams use other slots, and a launch captured into a
  *   graph, or on a stream beyond the slots, uses none (one workgroup per row
  *   tile).  Calls on different streams may run concurrently as long as their
- *   output buffers do not overlap.
+ *   output buffers do not overlap.  A slot belongs to the stream handle: let
+ *   a stream's pulsar_phase1_attn launches finish (hipStreamSynchronize)
+ *   before destroying it, since a stream created later may get the same
+ *   handle and with it the slot.
  */
 #ifndef PULSAR_H_
 #define PULSAR_H_
