@@ -166,16 +166,37 @@ size_t pulsar_maxidf_workspace_bytes(int batch, int64_t L, int num_blocks, int c
  * ids, sel_chunks  as for pulsar_maxidf_summaries.
  * chunk_scores     out float [batch, num_blocks, Lb / chunk], nullable.
  * scorer           a pulsar_scorer.
+ * workspace        device buffer of at least pulsar_chunk_workspace_bytes(...)
+ *                  bytes, 16-byte aligned, contents on entry irrelevant; or
+ *                  NULL.  With it, a small batch runs split over the blocks
+ *                  and the vocabulary (the Max-IDF split path's presence and
+ *                  df launches, then one workgroup per block); with NULL (or
+ *                  a size query of 0) one workgroup takes each sequence.  The
+ *                  scores agree bit for bit except where an fp64 sum taken
+ *                  in another order rounds to the other side of an fp32
+ *                  midpoint (one ulp), and the selections follow the scores.
  *
  * EINVAL: as for pulsar_maxidf_summaries, or an unknown scorer.
  * EUNSUPPORTED: num_blocks > 16, chunk not a power of two in [4, 256], or
  *         the df table, chunk keys and (BM25, ENTROPY) a 16 KB staging area
  *         do not fit in 160 KB of local data share (vocab up to about
  *         130,000 at chunk 32 and L = 128K for BM25 and ENTROPY).
+ * EWORKSPACE: a workspace smaller than the size query or misaligned.
  */
 int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
                            int topk, int vocab, int scorer, int32_t* sel_chunks,
-                           float* chunk_scores, void* stream);
+                           float* chunk_scores, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * Device workspace, in bytes, with which pulsar_chunk_summaries spreads a
+ * small batch over many compute units (the layout of
+ * pulsar_maxidf_workspace_bytes, for shapes whose score workgroup also fits
+ * its df table, chunk keys and staging in local data share); 0 when the
+ * shapes take one workgroup per sequence.  Host-only.
+ */
+size_t pulsar_chunk_workspace_bytes(int batch, int64_t L, int num_blocks, int chunk, int vocab,
+                                    int scorer);
 
 /*
  * Number of rows n_i of block i's Phase-1 input (Eq. 3; Appendix

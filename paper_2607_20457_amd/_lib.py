@@ -21,7 +21,8 @@ SIGNATURES = {
                                          _vp, _vp, _vp, _vp, _c_size, _vp]),
     "pulsar_maxidf_workspace_bytes": (_c_size, [_c_int, _c_i64, _c_int, _c_int, _c_int]),
     "pulsar_chunk_summaries": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
-                                        _c_int, _vp, _vp, _vp]),
+                                        _c_int, _vp, _vp, _vp, _c_size, _vp]),
+    "pulsar_chunk_workspace_bytes": (_c_size, [_c_int, _c_i64, _c_int, _c_int, _c_int, _c_int]),
     "pulsar_phase1_len": (_c_i64, [_c_i64, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int]),
     "pulsar_phase1_positions": (_c_int, [_vp, _c_int, _c_i64, _c_int, _c_int, _c_int, _c_int,
                                          _c_int, _c_int, _vp, _vp]),

@@ -79,10 +79,17 @@ def maxidf_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, 
     return out[0] if len(out) == 1 else tuple(out)
 
 
+def chunk_workspace_bytes(batch: int, L: int, num_blocks: int, chunk: int, vocab: int,
+                          scorer: int) -> int:
+    return int(_lib.lib().pulsar_chunk_workspace_bytes(batch, L, num_blocks, chunk, vocab, scorer))
+
+
 def chunk_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, vocab: int,
-                    scorer: int, return_scores: bool = False):
+                    scorer: int, return_scores: bool = False, workspace="auto"):
     """Top-k chunks per block under a scorer (SCORE_*).  ids int32 [batch, L]
-    -> sel int32 [batch, num_blocks, topk] (+ fp32 scores [batch, N, C])."""
+    -> sel int32 [batch, num_blocks, topk] (+ fp32 scores [batch, N, C]).
+    workspace: "auto" allocates the split path's workspace when the shapes
+    use one, None runs one workgroup per sequence, or a device buffer."""
     if ids.dim() == 1:
         ids = ids[None]
     _need(ids, torch.int32, "ids")
@@ -92,8 +99,14 @@ def chunk_summaries(ids: torch.Tensor, num_blocks: int, chunk: int, topk: int, v
     sel = torch.empty((batch, num_blocks, topk), dtype=torch.int32, device=dev)
     scores = torch.empty((batch, num_blocks, C), dtype=torch.float32, device=dev) \
         if return_scores else None
+    need = chunk_workspace_bytes(batch, L, num_blocks, chunk, vocab, scorer) \
+        if num_blocks > 0 else 0
+    if isinstance(workspace, str):
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need else None
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     st = _lib.lib().pulsar_chunk_summaries(_ptr(ids), batch, L, num_blocks, chunk, topk, vocab,
-                                           scorer, _ptr(sel), _ptr(scores), _stream())
+                                           scorer, _ptr(sel), _ptr(scores), _ptr(workspace),
+                                           ws_bytes, _stream())
     _lib.check(st, "pulsar_chunk_summaries")
     return (sel, scores) if return_scores else sel
 

@@ -120,9 +120,23 @@ int pulsar_maxidf_summaries(const int32_t* ids, int batch, int64_t L, int num_bl
                        lds, (hipStream_t)stream);
 }
 
+size_t pulsar_chunk_workspace_bytes(int batch, int64_t L, int num_blocks, int chunk, int vocab,
+                                    int scorer) {
+  // 0 wherever pulsar_chunk_summaries would refuse the shapes
+  if (scorer < PULSAR_SCORE_MAXIDF || scorer > PULSAR_SCORE_ENTROPY || num_blocks > 16 ||
+      num_blocks < 1 || chunk < 4 || !is_pow2(chunk) || vocab < 1 || L < 1 ||
+      scorer_lds_bytes(L, num_blocks, chunk, vocab, scorer) > PULSAR_LDS_BYTES)
+    return 0;
+  const size_t need = maxidf_split_workspace(batch, L, num_blocks, chunk, vocab);
+  if (need == 0 || scorer_split_lds_bytes(L, num_blocks, chunk, vocab, scorer) > PULSAR_LDS_BYTES)
+    return 0;
+  return need;
+}
+
 int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
                            int topk, int vocab, int scorer, int32_t* sel_chunks,
-                           float* chunk_scores, void* stream) {
+                           float* chunk_scores, void* workspace, size_t workspace_bytes,
+                           void* stream) {
   if (batch < 0 || L < 0 || num_blocks < 1 || vocab < 1 || chunk < 1 || topk < 0)
     return PULSAR_EINVAL;
   if (scorer < PULSAR_SCORE_MAXIDF || scorer > PULSAR_SCORE_ENTROPY) return PULSAR_EINVAL;
@@ -136,6 +150,12 @@ int pulsar_chunk_summaries(const int32_t* ids, int batch, int64_t L, int num_blo
   if (scorer_lds_bytes(L, num_blocks, chunk, vocab, scorer) > PULSAR_LDS_BYTES)
     return PULSAR_EUNSUPPORTED;
   if ((int64_t)batch * L == 0) return PULSAR_OK;
+  const size_t need = pulsar_chunk_workspace_bytes(batch, L, num_blocks, chunk, vocab, scorer);
+  if (need > 0 && workspace != nullptr) {
+    if (workspace_bytes < need || !aligned16(workspace)) return PULSAR_EWORKSPACE;
+    return launch_scorer_split(ids, batch, L, num_blocks, chunk, topk, vocab, scorer, sel_chunks,
+                               chunk_scores, workspace, (hipStream_t)stream);
+  }
   return launch_scorer(ids, batch, L, num_blocks, chunk, topk, vocab, scorer, sel_chunks,
                        chunk_scores, (hipStream_t)stream);
 }

@@ -174,6 +174,12 @@ int launch_decode(const uint16_t* q, const uint16_t* K, const uint16_t* V, int n
 int launch_scorer(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk, int topk,
                   int vocab, int scorer, int32_t* sel, float* scores, hipStream_t stream);
 size_t scorer_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab, int scorer);
+// The scorers' split path for a small batch (the workspace of
+// maxidf_split_workspace): LDS of its score kernel, and the launch.
+size_t scorer_split_lds_bytes(int64_t L, int num_blocks, int chunk, int vocab, int scorer);
+int launch_scorer_split(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                        int topk, int vocab, int scorer, int32_t* sel, float* scores,
+                        void* workspace, hipStream_t stream);
 
 int launch_positions(const RowMap& mp, const int32_t* sel, int64_t sel_bstride, int batch,
                      int n_rows, int32_t* pos, hipStream_t stream);

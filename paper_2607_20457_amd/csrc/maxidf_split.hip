@@ -30,25 +30,13 @@
 //
 // Workspace per sequence: N bitmaps of W = ceil(V / 32) words (padded to 32
 // bytes), then the df table of 32 W bytes (16 W of them used by nibbles).
-#include "summary.hpp"
+#include "split.hpp"
 
 namespace {
 
-constexpr int kSplitThreads = 1024;
 constexpr int kDfThreads = 256;
 constexpr int kMaxidfSplitBatch = 16;  // beyond this, one workgroup per sequence is as fast
 constexpr int kU = 8;                  // loads in flight per thread
-
-__host__ __device__ inline int64_t split_words(int vocab) { return ((int64_t)vocab + 31) / 32; }
-__host__ __device__ inline int64_t split_df_bytes(int vocab) { return split_words(vocab) * 32; }
-// the bitmaps, padded to 32 bytes so that the df table (and the next
-// sequence) stays 32-byte aligned
-__host__ __device__ inline int64_t split_bits_bytes(int num_blocks, int vocab) {
-  return ((int64_t)num_blocks * split_words(vocab) * 4 + 31) & ~int64_t(31);
-}
-__host__ __device__ inline int64_t split_seq_bytes(int num_blocks, int vocab) {
-  return split_bits_bytes(num_blocks, vocab) + split_df_bytes(vocab);
-}
 
 // Block j of sequence b: its ids set bits of a zeroed LDS bitmap (atomic
 // OR; bit t of word t / 32), which is then copied out as P_j.
@@ -226,20 +214,6 @@ __global__ __launch_bounds__(kDfThreads) void split_df_kernel(int num_blocks, in
   }
 }
 
-// Copy of n 16-byte units (K rounds of kSplitThreads, n > (K - 1) *
-// kSplitThreads) from global memory into LDS: all K loads are issued before
-// the first store.  Lanes past the end copy the last unit onto itself, so no
-// lane branches on its own load or store.
-template <int K>
-__device__ __forceinline__ void copy_rounds(const uint4* __restrict__ src, uint4* dst, int n,
-                                            int tid) {
-  uint4 r[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) r[k] = src[min(k * kSplitThreads + tid, n - 1)];
-#pragma unroll
-  for (int k = 0; k < K; ++k) dst[min(k * kSplitThreads + tid, n - 1)] = r[k];
-}
-
 // Block j of sequence b: the df of each id, each chunk's minimum, the top-k
 // chunks.  In round r thread tid holds the 8 consecutive ids
 // 8 (1024 r + tid) .. +7 of the block (two 16-byte groups), so a chunk of m
@@ -278,23 +252,7 @@ __global__ __launch_bounds__(kSplitThreads) void split_select_kernel(
   int4 q[2];
   load(0, q);
   if constexpr (DF_LDS) {
-    // as many rounds of 16-byte units as the table needs (it fits in LDS,
-    // so at most PULSAR_LDS_BYTES / 16 / kSplitThreads = 10)
-    static_assert(PULSAR_LDS_BYTES / 16 / kSplitThreads == 10, "copy rounds below");
-    const uint4* src = reinterpret_cast<const uint4*>(df);
-    uint4* dst = reinterpret_cast<uint4*>(lds);
-    switch ((tab16 + kSplitThreads - 1) / kSplitThreads) {
-      case 1: copy_rounds<1>(src, dst, tab16, tid); break;
-      case 2: copy_rounds<2>(src, dst, tab16, tid); break;
-      case 3: copy_rounds<3>(src, dst, tab16, tid); break;
-      case 4: copy_rounds<4>(src, dst, tab16, tid); break;
-      case 5: copy_rounds<5>(src, dst, tab16, tid); break;
-      case 6: copy_rounds<6>(src, dst, tab16, tid); break;
-      case 7: copy_rounds<7>(src, dst, tab16, tid); break;
-      case 8: copy_rounds<8>(src, dst, tab16, tid); break;
-      case 9: copy_rounds<9>(src, dst, tab16, tid); break;
-      default: copy_rounds<10>(src, dst, tab16, tid); break;
-    }
+    copy_to_lds(reinterpret_cast<const uint4*>(df), reinterpret_cast<uint4*>(lds), tab16, tid);
     // the first ids arrive before the barrier, not after it
     asm volatile("" : "+v"(q[0].x), "+v"(q[0].y), "+v"(q[0].z), "+v"(q[0].w), "+v"(q[1].x),
                  "+v"(q[1].y), "+v"(q[1].z), "+v"(q[1].w));
@@ -359,11 +317,8 @@ size_t maxidf_split_workspace(int batch, int64_t L, int num_blocks, int chunk, i
   return (size_t)(batch * split_seq_bytes(num_blocks, vocab));
 }
 
-int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
-                        int topk, int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf,
-                        void* workspace, hipStream_t stream) {
-  int chunk_log2 = 0;
-  while ((1 << chunk_log2) < chunk) ++chunk_log2;
+int launch_split_df(const int32_t* ids, int batch, int64_t L, int num_blocks, int vocab,
+                    float* idf, void* workspace, hipStream_t stream) {
   const int Lb = (int)(L / num_blocks);
   const int64_t seq_bytes = split_seq_bytes(num_blocks, vocab);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -388,7 +343,6 @@ int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks
   const dim3 dgrid((unsigned)(batch * slices));
   // counter planes: enough bits for num_blocks (<= 255); a nibble table for
   // up to 16 blocks
-  const bool nib = num_blocks <= 16;
   if (num_blocks < 16)
     hipLaunchKernelGGL((split_df_kernel<4, true>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
                        vocab, slices, ws, seq_bytes, idf);
@@ -401,7 +355,20 @@ int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks
   else
     hipLaunchKernelGGL((split_df_kernel<8, false>), dgrid, dim3(kDfThreads), 0, stream, num_blocks,
                        vocab, slices, ws, seq_bytes, idf);
-  if (hipGetLastError() != hipSuccess) return PULSAR_EHIP;
+  return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
+}
+
+int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks, int chunk,
+                        int topk, int vocab, int32_t* sel, int32_t* chunk_mindf, float* idf,
+                        void* workspace, hipStream_t stream) {
+  int chunk_log2 = 0;
+  while ((1 << chunk_log2) < chunk) ++chunk_log2;
+  const int Lb = (int)(L / num_blocks);
+  const int64_t seq_bytes = split_seq_bytes(num_blocks, vocab);
+  const int64_t grid = (int64_t)batch * num_blocks;
+  int st = launch_split_df(ids, batch, L, num_blocks, vocab, idf, workspace, stream);
+  if (st != PULSAR_OK) return st;
+  const bool nib = num_blocks <= 16;
   const size_t cl = (size_t)(Lb >> chunk_log2) * 4;
   const size_t df_tab = (size_t)split_words(vocab) * (nib ? 16 : 32);
   const bool df_lds = df_tab + cl <= PULSAR_LDS_BYTES;
@@ -412,6 +379,7 @@ int launch_maxidf_split(const int32_t* ids, int batch, int64_t L, int num_blocks
       hipSuccess)
     return PULSAR_EHIP;
   hipLaunchKernelGGL(sk, dim3((unsigned)grid), dim3(kSplitThreads), sl, stream, ids, L, num_blocks,
-                     Lb, chunk_log2, topk, vocab, ws, seq_bytes, sel, chunk_mindf);
+                     Lb, chunk_log2, topk, vocab, static_cast<const uint8_t*>(workspace), seq_bytes,
+                     sel, chunk_mindf);
   return hipGetLastError() == hipSuccess ? PULSAR_OK : PULSAR_EHIP;
 }

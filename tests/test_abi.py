@@ -256,10 +256,28 @@ def test_maxidf_workspace_sizes():
     assert ws(1, 4097, 4, 16, 100) == 0            # invalid shapes take no workspace
 
 
+def test_chunk_workspace_sizes():
+    ws = _lib.lib().pulsar_chunk_workspace_bytes
+    mx = _lib.lib().pulsar_maxidf_workspace_bytes
+    # the Max-IDF split path's layout, for every scorer
+    for scorer in range(4):
+        assert ws(1, 131072, 16, 32, 128256, scorer) == mx(1, 131072, 16, 32, 128256)
+        assert ws(16, 131072, 16, 32, 128256, scorer) == mx(16, 131072, 16, 32, 128256)
+        assert ws(17, 131072, 16, 32, 128256, scorer) == 0
+    assert ws(1, 131072, 1, 32, 128256, 1) == 0       # one block: nothing to split
+    assert ws(1, 131072, 17, 32, 128256, 1) == 0      # the scorers take at most 16 blocks
+    assert ws(1, 131072, 16, 32, 128256, 4) == 0      # unknown scorer
+    assert ws(1, 131072, 16, 24, 128256, 1) == 0      # chunk not a power of two
+    # no size where the call itself is unsupported (BM25's one-workgroup
+    # layout beyond LDS), while TF-IDF, which stages nothing, still fits
+    assert ws(1, 131072, 16, 32, 140000, 2) == 0
+    assert ws(1, 131072, 16, 32, 140000, 1) > 0
+
+
 def test_chunk_summaries_validation():
     f = _lib.lib().pulsar_chunk_summaries
     def call(ids=FAKE, batch=1, L=4096, N=4, m=16, k=4, V=1000, scorer=1, sel=FAKE):
-        return f(ids, batch, L, N, m, k, V, scorer, sel, None, None)
+        return f(ids, batch, L, N, m, k, V, scorer, sel, None, None, 0, None)
     assert call(scorer=4) == EINVAL and call(scorer=-1) == EINVAL
     assert call(L=4097) == EINVAL          # L % N
     assert call(m=24) == EINVAL            # Lb % m
@@ -271,3 +289,8 @@ def test_chunk_summaries_validation():
     assert call(m=512, L=8192, k=1) == EUNSUP
     assert call(L=131072, N=16, m=32, k=4, V=150000, scorer=2) == EUNSUP  # LDS
     assert call(batch=0, ids=None, sel=None) == 0
+    # a workspace below the size query
+    need = _lib.lib().pulsar_chunk_workspace_bytes(1, 4096, 4, 16, 1000, 1)
+    assert need > 0
+    assert f(FAKE, 1, 4096, 4, 16, 4, 1000, 1, FAKE, None, FAKE, need - 1, None) == EWS
+    assert f(FAKE, 1, 4096, 4, 16, 4, 1000, 1, FAKE, None, FAKE + 8, need, None) == EWS

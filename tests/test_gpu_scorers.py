@@ -26,24 +26,30 @@ NAMES = {P.SCORE_TFIDF: "tfidf", P.SCORE_BM25: "bm25", P.SCORE_ENTROPY: "entropy
 
 
 def _check(ids, N, m, k, V, scorer):
-    print(f"scorer parity: {NAMES[scorer]} batch={ids.shape[0]} L={ids.shape[1]} N={N} m={m} "
-          f"k={k} V={V}", flush=True)
+    """Both paths against the oracle: with the size query's workspace (split
+    over blocks and vocabulary where the shapes allow) and without one (one
+    workgroup per sequence)."""
     sel_ref, s_ref, amb = scorers.chunk_summaries(ids, N, m, k, V, scorer)
-    sel, s = P.chunk_summaries(to_dev_i32(ids), N, m, k, V, scorer, return_scores=True)
-    torch.cuda.synchronize()
-    sel, s = sel.cpu().numpy(), s.cpu().numpy()
-    exact = ~amb
-    assert np.array_equal(s[exact].view(np.uint32), s_ref[exact].view(np.uint32)), \
-        f"{NAMES[scorer]}: fp32 scores differ on {(s[exact] != s_ref[exact]).sum()} chunks"
-    if amb.any():
-        d = np.abs(s[amb].view(np.int32).astype(np.int64) - s_ref[amb].view(np.int32))
-        assert d.max() <= 1
-    if np.array_equal(s.view(np.uint32), s_ref.view(np.uint32)):
-        assert np.array_equal(sel, sel_ref)
-    else:
-        for bb in range(ids.shape[0]):
-            for j in range(N):
-                assert sel[bb, j].tolist() == scorers.select_by_score(s[bb, j], k)
+    d_ids = to_dev_i32(ids)
+    need = P.chunk_workspace_bytes(ids.shape[0], ids.shape[1], N, m, V, scorer)
+    for ws in ("auto", None) if need else (None,):
+        print(f"scorer parity: {NAMES[scorer]} batch={ids.shape[0]} L={ids.shape[1]} N={N} m={m} "
+              f"k={k} V={V} path={'split' if ws else 'one workgroup per sequence'}", flush=True)
+        sel, s = P.chunk_summaries(d_ids, N, m, k, V, scorer, return_scores=True, workspace=ws)
+        torch.cuda.synchronize()
+        sel, s = sel.cpu().numpy(), s.cpu().numpy()
+        exact = ~amb
+        assert np.array_equal(s[exact].view(np.uint32), s_ref[exact].view(np.uint32)), \
+            f"{NAMES[scorer]}: fp32 scores differ on {(s[exact] != s_ref[exact]).sum()} chunks"
+        if amb.any():
+            d = np.abs(s[amb].view(np.int32).astype(np.int64) - s_ref[amb].view(np.int32))
+            assert d.max() <= 1
+        if np.array_equal(s.view(np.uint32), s_ref.view(np.uint32)):
+            assert np.array_equal(sel, sel_ref)
+        else:
+            for bb in range(ids.shape[0]):
+                for j in range(N):
+                    assert sel[bb, j].tolist() == scorers.select_by_score(s[bb, j], k)
     return sel, s
 
 
@@ -69,6 +75,14 @@ def test_chunk_sizes(scorer, m):
 def test_discriminative_vocab_batch(scorer):
     ids = np.stack([workload.zipf_ids(1200 + b, 32768, 512) for b in range(3)])
     _check(ids, 8, 32, 16, 512, scorer)
+
+
+@pytest.mark.parametrize("scorer", SCORERS)
+def test_split_path_batch16(scorer):
+    # the largest batch the split path takes, 16 blocks (a nibble df table)
+    ids = np.stack([workload.zipf_ids(1300 + b, 16384, 3000) for b in range(16)])
+    assert P.chunk_workspace_bytes(16, 16384, 16, 16, 3000, scorer) > 0
+    _check(ids, 16, 16, 7, 3000, scorer)
 
 
 @pytest.mark.parametrize("scorer", SCORERS)
