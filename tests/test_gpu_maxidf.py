@@ -202,3 +202,37 @@ def test_split_path_large_vocab():
     # 24 blocks and a df byte table too large for LDS: looked up in the workspace
     ids = np.stack([workload.zipf_ids(6102 + b, 49152, 300000) for b in range(2)])
     _check(ids, 24, 32, 5, 300000, single=False)
+
+
+def test_split_path_in_a_graph_replays():
+    # The split path keeps no state outside the caller's workspace: captured
+    # into a graph, every replay equals the eager result bit for bit, with
+    # eager calls on other ids (through the same workspace) between them.
+    cfg = workload.CONFIGS["llama8b_128k"]
+    N, m, k, V = cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab
+    ids = to_dev_i32(workload.make_ids(cfg, batch=2))
+    other = to_dev_i32(np.stack([workload.zipf_ids(7000 + b, cfg.L, V) for b in range(2)]))
+    ws = torch.empty(P.maxidf_workspace_bytes(2, cfg.L, N, m, V), dtype=torch.uint8, device="cuda")
+    assert ws.numel() > 0
+    eager = P.maxidf_summaries(ids, N, m, k, V, return_mindf=True, return_idf=True, workspace=ws)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up outside the capture
+        P.maxidf_summaries(ids, N, m, k, V, return_mindf=True, return_idf=True, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        captured = P.maxidf_summaries(ids, N, m, k, V, return_mindf=True, return_idf=True,
+                                      workspace=ws)
+    for rep in range(3):
+        print(f"maxidf split graph replay {rep}", flush=True)
+        for t in captured:
+            t.fill_(-1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(captured, eager):
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32)), f"replay {rep}"
+        P.maxidf_summaries(other, N, m, k, V, return_mindf=True, workspace=ws)
+        torch.cuda.synchronize()

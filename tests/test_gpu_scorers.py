@@ -117,3 +117,37 @@ def test_planted_needles(scorer):
     sel, _ = _check(ids[None], 8, 32, 16, 1024, scorer)
     if scorer == P.SCORE_MAXIDF:
         assert all((p % 4096) // 32 in sel[0, p // 4096] for p in pos)
+
+
+def test_split_path_in_a_graph_replays():
+    # As for Max-IDF: captured into a graph, the split scorer path's replays
+    # equal the eager result bit for bit, with eager calls between them.
+    cfg = workload.CONFIGS["llama8b_32k"]
+    N, m, k, V = cfg.num_blocks, cfg.chunk, cfg.topk, cfg.vocab
+    ids = to_dev_i32(workload.make_ids(cfg, batch=2))
+    other = to_dev_i32(np.stack([workload.zipf_ids(7100 + b, cfg.L, V) for b in range(2)]))
+    need = P.chunk_workspace_bytes(2, cfg.L, N, m, V, P.SCORE_BM25)
+    assert need > 0
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    eager = P.chunk_summaries(ids, N, m, k, V, P.SCORE_BM25, return_scores=True, workspace=ws)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up outside the capture
+        P.chunk_summaries(ids, N, m, k, V, P.SCORE_BM25, return_scores=True, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        captured = P.chunk_summaries(ids, N, m, k, V, P.SCORE_BM25, return_scores=True,
+                                     workspace=ws)
+    for rep in range(3):
+        print(f"scorer split graph replay {rep}", flush=True)
+        for t in captured:
+            t.fill_(-1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(captured, eager):
+            assert torch.equal(a.view(torch.int32), b.view(torch.int32)), f"replay {rep}"
+        P.chunk_summaries(other, N, m, k, V, P.SCORE_ENTROPY, workspace=ws)
+        torch.cuda.synchronize()
