@@ -225,6 +225,26 @@ def test_phase2_query_noalloc_validation():
     assert lib.pulsar_phase2_query_workspace_bytes(16, 64, 8192, 0, 32, 8, 128) <= limit
 
 
+def test_phase1_positions_validation():
+    f = _lib.lib().pulsar_phase1_positions
+    def call(sel=FAKE, batch=1, L=4096, N=4, i=2, s=16, m=16, k=4, mode=0, pos=FAKE):
+        return f(sel, batch, L, N, i, s, m, k, mode, pos, None)
+    assert call(L=4097) == EINVAL                    # L % N
+    assert call(i=4) == EINVAL and call(i=-1) == EINVAL
+    assert call(s=2000) == EINVAL                    # sink beyond the block
+    assert call(m=16, k=65) == EINVAL                # topk * chunk beyond the block
+    assert call(mode=7) == EINVAL
+    assert call(batch=-1) == EINVAL
+    assert call(L=1 << 31, N=1, i=0, s=0, k=0) == EINVAL
+    assert call(pos=None) == EINVAL
+    assert call(sel=None) == EINVAL                  # Max-IDF prefix of an i > 0 block
+    assert call(batch=0, sel=None, pos=None) == 0    # nothing to write
+    # no selections needed (these would launch, so only their refusals are
+    # checked here): anchor and Even-Spaced modes, block 0, k = 0
+    assert call(sel=None, pos=None, mode=2) == EINVAL
+    assert call(sel=None, pos=None, i=0) == EINVAL
+
+
 def test_phase1_gather_validation():
     f = _lib.lib().pulsar_phase1_gather
     def call(X=FAKE, batch=1, L=4096, H=2, d=64, N=4, i=2, s=64, m=16, k=4, sel=FAKE, mode=0,
