@@ -44,7 +44,7 @@ extern "C" {
 typedef enum {
   PULSAR_OK = 0,
   PULSAR_EINVAL = -1,        /* an argument is out of range or a required pointer is NULL */
-  PULSAR_EUNSUPPORTED = -2,  /* valid by the paper's definition but outside what this build runs */
+  PULSAR_EUNSUPPORTED = -2,  /* valid by the paper's definition but outside what this library runs */
   PULSAR_EHIP = -3,          /* the HIP runtime reported an error at launch */
   PULSAR_EWORKSPACE = -4,    /* the workspace is NULL or smaller than the size query returned */
   PULSAR_ETOOLARGE = -5      /* the no-allocation call's partials exceed its static scratch */
