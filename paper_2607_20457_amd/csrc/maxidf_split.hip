@@ -7,13 +7,14 @@
 // the chip idle.  This path splits each sequence over its blocks and its
 // vocabulary, in three launches that communicate through a caller workspace:
 //
-//   presence  one workgroup per (sequence, block j): the block's ids write a
-//             1 into a zeroed LDS table of one byte per id (repeated ids
-//             write the same value, so plain byte stores suffice), which is
-//             packed into the workspace as P_j (bit t of word t / 32).  A
-//             vocabulary whose byte table exceeds LDS sets bits of an LDS
-//             bitmap with atomic OR instead.  Every word of P_j is written,
-//             so nothing needs clearing beforehand.
+//   presence  one workgroup per (sequence, block j, vocabulary slice): the
+//             block's ids in the slice write a 1 into a zeroed LDS table of
+//             one byte per id (repeated ids write the same value, so plain
+//             byte stores suffice; LDS atomic OR serialises on them), which
+//             is packed into the slice's words of P_j (bit t of word t / 32).
+//             Small batches take more slices, so that clearing and packing
+//             the tables is short; every slice reads the block's ids.  Every
+//             word of P_j is written, so nothing needs clearing beforehand.
 //   df        one thread per 32 ids: df(t) = sum_j P_j[t], counted with
 //             bit-sliced adders over the N words (one counter bit per plane),
 //             written to the workspace df table: nibbles df - 1 for N <= 16,
@@ -30,6 +31,8 @@
 //
 // Workspace per sequence: N bitmaps of W = ceil(V / 32) words (padded to 32
 // bytes), then the df table of 32 W bytes (16 W of them used by nibbles).
+#include <algorithm>
+
 #include "split.hpp"
 
 namespace {
@@ -38,47 +41,16 @@ constexpr int kDfThreads = 256;
 constexpr int kMaxidfSplitBatch = 16;  // beyond this, one workgroup per sequence is as fast
 constexpr int kU = 8;                  // loads in flight per thread
 
-// Block j of sequence b: its ids set bits of a zeroed LDS bitmap (atomic
-// OR; bit t of word t / 32), which is then copied out as P_j.
-__global__ __launch_bounds__(kSplitThreads) void split_presence_kernel(
-    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int vocab,
-    uint8_t* __restrict__ ws, int64_t seq_bytes) {
-  extern __shared__ __attribute__((aligned(16))) uint32_t bm[];
-  const int tid = threadIdx.x;
-  const int64_t b = blockIdx.x / num_blocks;
-  const int j = blockIdx.x - (int)(b * num_blocks);
-  const int W = (int)split_words(vocab);
-  const uint32_t vmax = (uint32_t)(vocab - 1);
-  for (int w = tid; w < W; w += kSplitThreads) bm[w] = 0u;
-  __syncthreads();
-  const int32_t* seq = ids + b * L + (int64_t)j * Lb;
-  // An id at or above vocab is the caller's error: clamped into the bitmap.
-  // kU ids per thread are loaded together before their atomics.
-  for (int x0 = 0; x0 < Lb; x0 += kU * kSplitThreads) {
-    uint32_t t[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int x = x0 + u * kSplitThreads + tid;
-      // a lane past the block re-reads the block's last id: marking it again
-      // changes nothing, and such lanes form no chunk (Lb is a multiple of
-      // the chunk); without a branch all kU loads are issued together
-      t[u] = min((uint32_t)seq[min(x, Lb - 1)], vmax);
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      atomicOr(&bm[t[u] >> 5], 1u << (t[u] & 31));
-  }
-  __syncthreads();
-  uint32_t* bits = reinterpret_cast<uint32_t*>(ws + b * seq_bytes) + (int64_t)j * W;
-  for (int w = tid; w < W; w += kSplitThreads) bits[w] = bm[w];
-}
-
-// Block j of sequence b with a byte per id: the block's ids write 1 into a
-// zeroed LDS byte table (repeated ids write the same value, so plain byte
-// stores suffice), then each 32 bytes are packed into the word of P_j.
-// Needs 32 W bytes of LDS.
+// Block j of sequence b (blockIdx.x = b N + j), vocabulary slice
+// s = blockIdx.y (words [s Ws, (s + 1) Ws) of the bitmap), with a byte per
+// id: the block's ids in the slice write 1 into a zeroed LDS byte table
+// (repeated ids write the same value, so plain byte stores suffice), then
+// each 32 bytes are packed into the word of P_j.  Slicing keeps the table
+// small, so that clearing and packing it are short; every slice reads the
+// block's ids.  Needs 32 Ws + 16 bytes of LDS: ids outside the slice write
+// the pad byte after the table, so the stores need no branch.
 __global__ __launch_bounds__(kSplitThreads) void split_presence_bytes_kernel(
-    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int vocab,
+    const int32_t* __restrict__ ids, int64_t L, int num_blocks, int Lb, int vocab, int Ws,
     uint8_t* __restrict__ ws, int64_t seq_bytes) {
   extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
   uint8_t* const pb = reinterpret_cast<uint8_t*>(lds);
@@ -87,6 +59,10 @@ __global__ __launch_bounds__(kSplitThreads) void split_presence_bytes_kernel(
   const int64_t b = blockIdx.x / num_blocks;
   const int j = blockIdx.x - (int)(b * num_blocks);
   const int W = (int)split_words(vocab);
+  const int w0 = blockIdx.y * Ws;
+  const int nw = max(0, min(W, w0 + Ws) - w0);  // words of this slice
+  const uint32_t t0 = 32u * (uint32_t)w0;       // its first id
+  const uint32_t span = 32u * (uint32_t)nw;
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const int32_t* seq = ids + b * L + (int64_t)j * Lb;
   auto load = [&](int x0, uint32_t (&t)[kU]) {
@@ -102,19 +78,21 @@ __global__ __launch_bounds__(kSplitThreads) void split_presence_bytes_kernel(
   // the first ids are in flight while the table is cleared
   uint32_t t[kU];
   load(0, t);
-  for (int w = tid; w < 2 * W; w += kSplitThreads) p16[w] = make_uint4(0u, 0u, 0u, 0u);
+  for (int w = tid; w < 2 * nw; w += kSplitThreads) p16[w] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
   for (int x0 = 0; x0 < Lb; x0 += kU * kSplitThreads) {
     if (x0 > 0) load(x0, t);
 #pragma unroll
-    for (int u = 0; u < kU; ++u)
-      pb[t[u]] = 1;
+    for (int u = 0; u < kU; ++u) {
+      const uint32_t r = t[u] - t0;  // wraps for ids below the slice
+      pb[min(r, span)] = 1;
+    }
   }
   __syncthreads();
   // byte k of a 4-byte group (0 or 1) lands on bit 24 + k of x * 0x01020408
   // (the other partial products fall on distinct bits below 24)
-  uint32_t* bits = reinterpret_cast<uint32_t*>(ws + b * seq_bytes) + (int64_t)j * W;
-  for (int w = tid; w < W; w += kSplitThreads) {
+  uint32_t* bits = reinterpret_cast<uint32_t*>(ws + b * seq_bytes) + (int64_t)j * W + w0;
+  for (int w = tid; w < nw; w += kSplitThreads) {
     const uint4 lo = p16[2 * w], hi = p16[2 * w + 1];
     const uint32_t g[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
     uint32_t v = 0;
@@ -323,21 +301,26 @@ int launch_split_df(const int32_t* ids, int batch, int64_t L, int num_blocks, in
   const int64_t seq_bytes = split_seq_bytes(num_blocks, vocab);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   const int64_t grid = (int64_t)batch * num_blocks;
-  const size_t bytes_tab = (size_t)split_words(vocab) * 32;
-  if (bytes_tab <= PULSAR_LDS_BYTES) {
-    if (hipFuncSetAttribute((const void*)split_presence_bytes_kernel,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes_tab) != hipSuccess)
-      return PULSAR_EHIP;
-    hipLaunchKernelGGL(split_presence_bytes_kernel, dim3((unsigned)grid), dim3(kSplitThreads),
-                       bytes_tab, stream, ids, L, num_blocks, Lb, vocab, ws, seq_bytes);
-  } else {
-    const size_t tab = (size_t)split_words(vocab) * 4;
-    if (hipFuncSetAttribute((const void*)split_presence_kernel,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)tab) != hipSuccess)
-      return PULSAR_EHIP;
-    hipLaunchKernelGGL(split_presence_kernel, dim3((unsigned)grid), dim3(kSplitThreads), tab,
-                       stream, ids, L, num_blocks, Lb, vocab, ws, seq_bytes);
-  }
+  // Vocabulary slices: enough for the byte table to fit in LDS; for a grid
+  // of at most 32 workgroups, more (down to 512-word slices) while it stays
+  // within one workgroup per CU.  (Larger grids gain nothing from slicing
+  // once their ids come from HBM: every slice reads the block's ids.)
+  constexpr int kSliceWords = 512;
+  const int64_t W = split_words(vocab);
+  const int64_t max_ws = (PULSAR_LDS_BYTES - 16) / 32;  // words of the largest table
+  const int64_t fit = (W + max_ws - 1) / max_ws;
+  const int64_t small = (W + kSliceWords - 1) / kSliceWords;
+  const int64_t room = grid <= 32 ? 256 / grid : 1;
+  const int vslices = (int)std::max(fit, std::min(small, room));
+  const int64_t Ws = (W + vslices - 1) / vslices;
+  const size_t bytes_tab = (size_t)Ws * 32 + 16;  // at most the LDS, by the choice of `fit`
+  if (bytes_tab > PULSAR_LDS_BYTES) return PULSAR_EUNSUPPORTED;
+  if (hipFuncSetAttribute((const void*)split_presence_bytes_kernel,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes_tab) != hipSuccess)
+    return PULSAR_EHIP;
+  hipLaunchKernelGGL(split_presence_bytes_kernel, dim3((unsigned)grid, (unsigned)vslices),
+                     dim3(kSplitThreads), bytes_tab, stream, ids, L, num_blocks, Lb, vocab, (int)Ws,
+                     ws, seq_bytes);
   if (hipGetLastError() != hipSuccess) return PULSAR_EHIP;
   const int slices = (int)((split_words(vocab) + kDfThreads - 1) / kDfThreads);
   const dim3 dgrid((unsigned)(batch * slices));
