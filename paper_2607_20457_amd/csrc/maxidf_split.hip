@@ -291,7 +291,8 @@ size_t maxidf_split_workspace(int batch, int64_t L, int num_blocks, int chunk, i
     return 0;
   const int64_t Lb = L / num_blocks;
   if (Lb % chunk != 0 || Lb / chunk > 16384 || L >= ((int64_t)1 << 31)) return 0;
-  if (split_words(vocab) * 4 > PULSAR_LDS_BYTES) return 0;  // the presence bitmap
+  // vocab up to 1310720 (40960 words): at most 9 presence slices per block
+  if (split_words(vocab) * 4 > PULSAR_LDS_BYTES) return 0;
   return (size_t)(batch * split_seq_bytes(num_blocks, vocab));
 }
 

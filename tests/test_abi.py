@@ -271,8 +271,8 @@ def test_maxidf_workspace_sizes():
     assert ws(16, 131072, 16, 32, 128256) == 16 * one
     assert ws(17, 131072, 16, 32, 128256) == 0     # one workgroup per sequence is as fast
     assert ws(1, 131072, 1, 32, 128256) == 0       # one block: nothing to split
-    assert ws(1, 131072, 16, 32, 200000) > 0       # bitmaps of vocab / 8 bytes in LDS
-    assert ws(1, 131072, 16, 32, 2000000) == 0     # presence bitmap beyond LDS
+    assert ws(1, 131072, 16, 32, 200000) > 0       # presence in vocabulary slices
+    assert ws(1, 131072, 16, 32, 2000000) == 0     # above the 1310720-id bound
     assert ws(1, 4097, 4, 16, 100) == 0            # invalid shapes take no workspace
 
 
