@@ -178,6 +178,7 @@ def test_every_kernel_layout(L, N, m, V, layout):
 
 @pytest.mark.parametrize("L,N,m,V,batch", [
     (131072, 16, 32, 128256, 16),   # the largest batch the split path takes
+    (131072, 16, 32, 128256, 2),    # 32 workgroups: the largest grid whose presence is sliced
     (32768, 32, 16, 32000, 12),     # 384 workgroups: more than the chip holds at once
     (8000, 8, 4, 700, 3),           # blocks of 1000 ids: not a multiple of the workgroup
     (65536, 4, 256, 5000, 2),       # chunks of 256 ids: minima across wavefronts
