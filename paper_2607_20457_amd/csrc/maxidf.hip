@@ -25,10 +25,11 @@
 //
 // Three kernels:
 //   * resident (vocab <= 131072, L = 8192 times a power of two up to 16,
-//     blocks of a multiple of 8192 ids, hence N <= 16): stamp code; pass 1
-//     keeps every thread's ids (up to 128) in registers, packed, and pass 2
-//     reads them back from there, so the ids cross HBM once; persistent over
-//     the batch, one workgroup per compute unit;
+//     blocks of a multiple of 8192 ids, hence N <= 16): stamp code (with df
+//     in the high nibble, see rstamp_tokens); pass 1 keeps every thread's
+//     ids (up to 128) in registers, packed, and pass 2 reads them back from
+//     there, so the ids cross HBM once; persistent over the batch, one
+//     workgroup per compute unit;
 //   * streaming, stamp code (N <= 16, table and chunk minima fit in LDS):
 //     pass 2 streams the ids from HBM a second time;
 //   * streaming, bitmaps: compact layout (vocab <= 131072: a fixed 4096-word
@@ -326,6 +327,37 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
   select_topk(cmin, b, num_blocks, Lb >> chunk_log2, (uint32_t)num_blocks, topk, sel, wave, lane);
 }
 
+// Stamp code of the resident kernel, block j: the high nibble of an id's byte
+// holds df - 1 and the low nibble the stamp 15 - j of the last block j it was
+// seen in; kStampNever (0xFF) before it is first seen.  The minimum of a
+// chunk's codes then carries the chunk's minimum df - 1 in its high nibble,
+// so pass 2 needs no conversion of the table.  A lane whose id is not yet
+// stamped with j writes (df - 1 + 1, 15 - j); as with stamp_tokens, every
+// writer of one byte during one block writes the same value.  CHECK_NEVER:
+// kStampNever carries the stamp of block 0 in its low nibble, so a round that
+// may belong to block 0 also tests for it.  nd: each id's df - 1 once this
+// block is counted (final in the last block).
+template <bool CHECK_NEVER>
+__device__ __forceinline__ void rstamp_tokens(const int (&t)[4], int j, uint8_t* code,
+                                              uint32_t (&nd)[4]) {
+  uint32_t c[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) c[i] = code[t[i]];
+  const uint32_t sj = 15u - (uint32_t)j;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bool stamped = (c[i] & 15u) == sj && (!CHECK_NEVER || c[i] != kStampNever);
+    const uint32_t nc = ((c[i] + 16u) & 0xF0u) | sj;  // 0xFF + 16 wraps to df - 1 = 0
+    nd[i] = (stamped ? c[i] : nc) >> 4;
+    if (!stamped) code[t[i]] = (uint8_t)nc;
+  }
+}
+
+// df of a resident stamp code (0 for an id never seen)
+__device__ __forceinline__ uint32_t rstamp_df(uint32_t c) {
+  return c == kStampNever ? 0u : (c >> 4) + 1u;
+}
+
 // Register-resident variant with the stamp code when the sequence fits the
 // register file: L = ROUNDS * 8192 with ROUNDS a power of two up to 16, and
 // Lb a multiple of 8192, so that every thread owns exactly ROUNDS x 2
@@ -350,8 +382,16 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_kernel(
 //
 // ROUNDS and the chunk's lane group (GL = log2(chunk / 4), or -1 for any)
 // are template arguments, so that the loops are straight-line code: every
-// load's wait is exact and the cross-lane minimum has no branches.
-template <int ROUNDS, int GL, bool CARRY_NEXT>
+// load's wait is exact and the cross-lane minimum has no branches.  ONE: one
+// round per block (Lb = 8192, N = ROUNDS), so the block of a round is known
+// at compile time: block 0 writes its codes without reading them (every id
+// is new), and the last block keeps each id's final df - 1 in the registers
+// of its packed ids, so pass 2 looks up only the other blocks.
+//
+// The table of the next sequence is cleared while the select of the current
+// one runs (the select reads only the chunk minima); the first sequence's,
+// while its first ids are loading.
+template <int ROUNDS, int GL, bool CARRY_NEXT, bool ONE>
 __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
     const int32_t* __restrict__ ids, int batch, int num_blocks, int rpb_log2, int chunk_log2,
     int topk, int vocab, int32_t* __restrict__ sel, int32_t* __restrict__ chunk_mindf,
@@ -369,7 +409,6 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
   const int wave = tid >> 6;
   uint8_t* const lds8 = reinterpret_cast<uint8_t*>(lds);
   uint8_t* code8 = lds8;
-  uint32_t* codew = lds;
   uint8_t* cmin = lds8 + kFastVocab;
   const uint32_t vmax = (uint32_t)(vocab - 1);
   const int vocab_w4 = (vocab + 3) >> 2;
@@ -392,30 +431,38 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
     }
   };
 
+  auto clear_table = [&]() {
+    const uint4 never = make_uint4(kStampNever * 0x01010101u, kStampNever * 0x01010101u,
+                                   kStampNever * 0x01010101u, kStampNever * 0x01010101u);
+    uint4* code16 = reinterpret_cast<uint4*>(lds);
+    for (int w = tid; w < (vocab_w4 + 3) >> 2; w += MAXIDF_THREADS) code16[w] = never;
+  };
   int4 nbuf[CARRY > 0 ? CARRY : 1][2];  // the next sequence's first CARRY rounds
+  int4 cbuf[PREFETCH + 1][2];           // the rounds in flight during pass 1
   {
+    // the first sequence's first rounds are in flight while its table is
+    // cleared (without CARRY_NEXT a workgroup has one sequence, and its
+    // first rounds are loaded here rather than in the loop)
     const __amdgpu_buffer_rsrc_t r0 = seq_rsrc(blockIdx.x);
 #pragma unroll
     for (int rd = 0; rd < CARRY; ++rd) load_round(r0, rd, nbuf[rd]);
+    if constexpr (!CARRY_NEXT) {
+#pragma unroll
+      for (int i = 0; i < PREFETCH && i < ROUNDS; ++i) load_round(r0, i, cbuf[i]);
+    }
+    clear_table();
   }
-
   for (int64_t b = blockIdx.x; b < batch; b += gridDim.x) {
     const __amdgpu_buffer_rsrc_t rsrc = seq_rsrc(b);
     const __amdgpu_buffer_rsrc_t rnext = seq_rsrc(b + gridDim.x);
 
     // ---- pass 1: document frequency, ids kept in registers ----------------
-    int4 cbuf[PREFETCH + 1][2];
     uint32_t plo[ROUNDS][2][2];              // low 16 bits, two ids per register
     uint32_t hb[(ROUNDS * 2 + 7) / 8] = {};  // bit 16 of the ids of slot s: bit s % 8 of each byte
-    // the first loads are in flight while the table is cleared
+    if constexpr (CARRY_NEXT) {
 #pragma unroll
-    for (int i = CARRY; i < CARRY + PREFETCH && i < ROUNDS; ++i)
-      load_round(rsrc, i, cbuf[i % (PREFETCH + 1)]);
-    {
-      const uint4 never = make_uint4(kStampNever * 0x01010101u, kStampNever * 0x01010101u,
-                                     kStampNever * 0x01010101u, kStampNever * 0x01010101u);
-      uint4* code16 = reinterpret_cast<uint4*>(lds);
-      for (int w = tid; w < (vocab_w4 + 3) >> 2; w += MAXIDF_THREADS) code16[w] = never;
+      for (int i = CARRY; i < CARRY + PREFETCH && i < ROUNDS; ++i)
+        load_round(rsrc, i, cbuf[i % (PREFETCH + 1)]);
     }
     __syncthreads();
 #pragma unroll
@@ -444,16 +491,35 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
         // packed here, not next to pass 2: the compiler would otherwise keep
         // the unpacked ids alive
         asm volatile("" : "+v"(plo[rd][u][0]), "+v"(plo[rd][u][1]), "+v"(hb[slot >> 3]));
-        stamp_tokens<4, false>(tk, j, vmax, code8);
+        if (ONE && rd == 0) {
+          // block 0: every id is seen for the first time (df 1, stamp of
+          // block 0), so its byte need not be read
+#pragma unroll
+          for (int i = 0; i < 4; ++i) code8[tk[i]] = (uint8_t)15u;
+          if (ROUNDS == 1) plo[rd][u][0] = 0u;
+        } else {
+          uint32_t nd[4];
+          if (ONE)
+            rstamp_tokens<false>(tk, j, code8, nd);
+          else
+            rstamp_tokens<true>(tk, j, code8, nd);
+          // the last block: the df - 1 read or written now is final, so
+          // pass 2 takes it from here instead of the table
+          if (ONE && rd == ROUNDS - 1)
+            plo[rd][u][0] = nd[0] | (nd[1] << 8) | (nd[2] << 16) | (nd[3] << 24);
+        }
       }
     }
     __syncthreads();
     if (idf) {
-      write_idf<true>(code8, vocab, num_blocks, idf + b * vocab, tid);
+      const float nb = (float)num_blocks;
+      float* out = idf + b * vocab;
+      for (int t = tid; t < vocab; t += MAXIDF_THREADS) {
+        const uint32_t d = rstamp_df(code8[t]);
+        out[t] = logf(nb / (float)(d > 1u ? d : 1u));
+      }
       __syncthreads();
     }
-    stamp_to_df(codew, vocab_w4, tid);
-    __syncthreads();
 
     // ---- pass 2: per-chunk minimum df from the registers ------------------
     // (the thread index is re-formed in every iteration: values derived from
@@ -474,8 +540,11 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
         const uint32_t t1 = __builtin_amdgcn_perm(x, lo0, 0x0C050302u);
         const uint32_t t2 = __builtin_amdgcn_perm(x, lo1, 0x0C060100u);
         const uint32_t t3 = __builtin_amdgcn_perm(x, lo1, 0x0C070302u);
-        mn[u] = min(min((uint32_t)code8[t0], (uint32_t)code8[t1]),
-                    min((uint32_t)code8[t2], (uint32_t)code8[t3]));
+        if (ONE && rd == ROUNDS - 1)
+          mn[u] = min(min(lo0 & 0xFFu, (lo0 >> 8) & 0xFFu), min((lo0 >> 16) & 0xFFu, lo0 >> 24));
+        else
+          mn[u] = min(min((uint32_t)code8[t0], (uint32_t)code8[t1]),
+                      min((uint32_t)code8[t2], (uint32_t)code8[t3])) >> 4;
       }
       const int g8 = rd * MAXIDF_THREADS + tid_i;  // the lane's 8-id group in the sequence
       if (cl2 == 2) {
@@ -505,6 +574,9 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
       }
     }
     __syncthreads();
+    // the next sequence's table is cleared while the select runs (it reads
+    // only the chunk minima)
+    if (b + gridDim.x < batch) clear_table();
     select_topk(cmin, b, num_blocks, (int)(L / num_blocks) >> chunk_log2, (uint32_t)num_blocks, topk,
                 sel, wave, lane);
   }
@@ -514,20 +586,25 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void maxidf_resident_kernel(
 // for chunks of 16 and 32 ids, the common sizes.
 typedef void (*ResidentKernel)(const int32_t*, int, int, int, int, int, int, int32_t*, int32_t*,
                                float*);
-template <int ROUNDS, bool CARRY_NEXT>
+template <int ROUNDS, bool CARRY_NEXT, bool ONE>
 static ResidentKernel resident_for_chunk(int chunk_log2) {
-  if (chunk_log2 == 5) return maxidf_resident_kernel<ROUNDS, 3, CARRY_NEXT>;
-  if (chunk_log2 == 4) return maxidf_resident_kernel<ROUNDS, 2, CARRY_NEXT>;
-  return maxidf_resident_kernel<ROUNDS, -1, CARRY_NEXT>;
+  if (chunk_log2 == 5) return maxidf_resident_kernel<ROUNDS, 3, CARRY_NEXT, ONE>;
+  if (chunk_log2 == 4) return maxidf_resident_kernel<ROUNDS, 2, CARRY_NEXT, ONE>;
+  return maxidf_resident_kernel<ROUNDS, -1, CARRY_NEXT, ONE>;
+}
+template <int ROUNDS, bool CARRY_NEXT>
+static ResidentKernel resident_for_chunk(int chunk_log2, int rpb_log2) {
+  return rpb_log2 == 0 ? resident_for_chunk<ROUNDS, CARRY_NEXT, true>(chunk_log2)
+                       : resident_for_chunk<ROUNDS, CARRY_NEXT, false>(chunk_log2);
 }
 template <bool CARRY_NEXT>
-static ResidentKernel resident_kernel(int rounds, int chunk_log2) {
+static ResidentKernel resident_kernel(int rounds, int chunk_log2, int rpb_log2) {
   switch (rounds) {
-    case 16: return resident_for_chunk<16, CARRY_NEXT>(chunk_log2);
-    case 8: return resident_for_chunk<8, CARRY_NEXT>(chunk_log2);
-    case 4: return resident_for_chunk<4, CARRY_NEXT>(chunk_log2);
-    case 2: return resident_for_chunk<2, CARRY_NEXT>(chunk_log2);
-    case 1: return resident_for_chunk<1, CARRY_NEXT>(chunk_log2);
+    case 16: return resident_for_chunk<16, CARRY_NEXT>(chunk_log2, rpb_log2);
+    case 8: return resident_for_chunk<8, CARRY_NEXT>(chunk_log2, rpb_log2);
+    case 4: return resident_for_chunk<4, CARRY_NEXT>(chunk_log2, rpb_log2);
+    case 2: return resident_for_chunk<2, CARRY_NEXT>(chunk_log2, rpb_log2);
+    case 1: return resident_for_chunk<1, CARRY_NEXT>(chunk_log2, rpb_log2);
     default: return nullptr;  // maxidf_plan admits only the round counts above
   }
 }
@@ -553,8 +630,8 @@ int launch_maxidf(const int32_t* ids, int batch, int64_t L, int num_blocks, int 
         n_cu < 1)
       return PULSAR_EHIP;
     const int grid = batch < n_cu ? batch : n_cu;
-    const ResidentKernel kern = batch > grid ? resident_kernel<true>(rounds, chunk_log2)
-                                             : resident_kernel<false>(rounds, chunk_log2);
+    const ResidentKernel kern = batch > grid ? resident_kernel<true>(rounds, chunk_log2, rpb_log2)
+                                             : resident_kernel<false>(rounds, chunk_log2, rpb_log2);
     if (kern == nullptr) return PULSAR_EINVAL;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(MAXIDF_THREADS), 0, stream, ids, batch, num_blocks,
                        rpb_log2, chunk_log2, topk, vocab, sel, chunk_mindf, idf);
