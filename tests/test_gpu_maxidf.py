@@ -83,6 +83,17 @@ def test_batch8_at_128k():
     _check(ids, cfg.num_blocks, cfg.chunk, 32, cfg.vocab, idf_too=False)
 
 
+@pytest.mark.parametrize("L,N,m", [(8192, 1, 32), (16384, 1, 16), (131072, 2, 32),
+                                   (131072, 8, 64), (32768, 4, 16)])
+def test_resident_block_layouts(L, N, m):
+    # The register-resident kernel with one round (8192 ids) per block, where
+    # block 0 is also the last block when N = 1, and with several rounds per
+    # block, where the first block's rounds test for never-seen ids.
+    ids = workload.zipf_ids(5000 + L // 8192 + N, L, 128256)[None]
+    print(f"maxidf resident: L={L} N={N} m={m}", flush=True)
+    _check(ids, N, m, min(6, L // N // m), 128256)
+
+
 def test_single_block_and_adversarial_contention():
     ids = workload.zipf_ids(9, 4096, 3000)[None]
     sel = _check(ids, 1, 16, 7, 3000)
@@ -144,7 +155,7 @@ def test_positions_ragged_shapes():
 
 
 @pytest.mark.parametrize("L,N,batch,m", [(131072, 16, 600, 32), (16384, 2, 700, 16),
-                                         (65536, 8, 520, 64)])
+                                         (65536, 8, 520, 64), (131072, 4, 300, 32)])
 def test_batch_beyond_compute_units(L, N, batch, m):
     # More sequences than compute units: each workgroup runs several of them
     # in turn and loads the next one's first ids while finishing the current
