@@ -142,6 +142,24 @@ def test_positions_match_eq3(mode):
             assert np.array_equal(pos[b], ref)
 
 
+@pytest.mark.parametrize("L,N,sink,m,k", [
+    (32768, 8, 64, 32, 16),        # sigma 512
+    (3000, 3, 40, 20, 7),          # sigma 140, blocks of 1000
+    (12000, 4, 5, 1, 3),           # sigma 3
+    (8000, 4, 0, 1, 1),            # sigma 1: each block's first position
+    (131072, 2, 64, 256, 255),     # sigma 65280: near the top of the 32-bit offset's range
+    (131072, 2, 64, 256, 256),     # sigma 65536 (= Lb): the 64-bit offset
+])
+def test_even_spaced_positions(L, N, sink, m, k):
+    # Even-Spaced prefix points j Lb + floor(p (Lb - 1) / (sigma - 1)) for
+    # every block, against the oracle's map (no selection is read)
+    print(f"even-spaced positions: L={L} N={N} sink={sink} m={m} k={k}", flush=True)
+    for i in range(N):
+        pos = P.phase1_positions(None, 1, L, N, i, sink, m, k, assembly.PREFIX_EVEN).cpu().numpy()
+        ref = assembly.phase1_positions(L, N, i, sink, m, k, None, assembly.PREFIX_EVEN)
+        assert np.array_equal(pos[0], ref)
+
+
 def test_positions_ragged_shapes():
     L, N, s, m, k = 3 * 1000, 3, 40, 20, 7
     rng = np.random.default_rng(4)
