@@ -94,6 +94,15 @@ def test_resident_block_layouts(L, N, m):
     _check(ids, N, m, min(6, L // N // m), 128256)
 
 
+def test_resident_tiny_vocabularies():
+    # every lane stamps the same few bytes: one id (df = N everywhere) and
+    # three ids, one of them absent from the last block
+    _check(np.zeros((1, 16384), dtype=np.int32), 2, 16, 5, 1)
+    ids = (np.arange(32768, dtype=np.int32) % 3)[None]
+    ids[0, 24576:] = np.where(ids[0, 24576:] == 2, 0, ids[0, 24576:])
+    _check(ids, 4, 32, 3, 3)
+
+
 def test_single_block_and_adversarial_contention():
     ids = workload.zipf_ids(9, 4096, 3000)[None]
     sel = _check(ids, 1, 16, 7, 3000)
