@@ -139,11 +139,13 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void scorer_kernel(
   const int nchunks_seq = (int)(L >> chunk_log2);
   int4* stage = reinterpret_cast<int4*>(lds8 + stage_off) + wave * 64;
   const int gbase = lane & ~(group - 1);  // first lane of this lane's chunk
-  for (int it = 0; it < n_iter; ++it) {  // the same trip count in every lane
+  // the next iteration's ids load while this one is scored; past the end a
+  // lane re-reads the last group (without a branch), which it does not use
+  auto load_it = [&](int it) { return seq4[min(it * MAXIDF_THREADS + tid, nvec_seq - 1)]; };
+  auto body = [&](int it, const int4 x4) {
     const int v = it * MAXIDF_THREADS + tid;
-    const int4 x4 = seq4[min(v, nvec_seq - 1)];
-    const uint32_t t[4] = {min((uint32_t)x4.x, vmax), min((uint32_t)x4.y, vmax),
-                           min((uint32_t)x4.z, vmax), min((uint32_t)x4.w, vmax)};
+    auto clamp = [&](int x) { return (uint32_t)x < vmax ? (uint32_t)x : vmax; };
+    const uint32_t t[4] = {clamp(x4.x), clamp(x4.y), clamp(x4.z), clamp(x4.w)};
     uint32_t dfm1[4];  // df - 1
 #pragma unroll
     for (int i = 0; i < 4; ++i) dfm1[i] = code8[t[i]];
@@ -203,6 +205,15 @@ __global__ __launch_bounds__(MAXIDF_THREADS) void scorer_kernel(
       keys[c] = key;
       if (scores) scores[b * nchunks_seq + c] = score;
     }
+  };
+  // unrolled by two, so that each buffer keeps its register while its load
+  // is in flight (the same trip count in every lane)
+  int4 xa = load_it(0), xb = load_it(1);
+  for (int it = 0; it < n_iter; it += 2) {
+    body(it, xa);
+    xa = load_it(it + 2);
+    if (it + 1 < n_iter) body(it + 1, xb);
+    xb = load_it(it + 3);
   }
   __syncthreads();
 
